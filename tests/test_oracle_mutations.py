@@ -1,0 +1,131 @@
+"""The pins must catch plausible mistakes in the oracle.
+
+Each case plants one mistake in a copy of an oracle module's source (an
+off-by-one in the causal mask, a dropped cache row, a dropped scale, a summary on
+the wrong side of its k-mer, a missing partial-k-mer summary, ...), loads the
+copy in place of the real module, and checks that at least one pin test fails.
+Everything runs on the CPU.
+"""
+
+import importlib.util
+import os
+import sys
+
+import pytest
+
+import oracle.attention
+import oracle.decode
+import oracle.layout
+import test_oracle_attention as TA
+import test_oracle_decode as TD
+import test_oracle_layout as TL
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _mutant(module, old, new):
+    path = module.__file__
+    src = open(path).read()
+    assert src.count(old) == 1, f"mutation anchor not unique in {path}: {old!r}"
+    spec = importlib.util.spec_from_loader(module.__name__ + "_mutant", loader=None,
+                                           origin=path)
+    mod = importlib.util.module_from_spec(spec)
+    mod.__package__ = "oracle"
+    exec(compile(src.replace(old, new), path, "exec"), mod.__dict__)
+    return mod
+
+
+def _layout_pins():
+    for case in TL._golden_cases():
+        TL.test_worked_examples(*case)
+    for seed in range(10):
+        TL.test_appendix_a_closed_forms(seed)
+        TL.test_kmer_membership_and_positions(seed)
+        TL.test_literal_string_insertion(seed)
+
+
+def _attention_pins():
+    for seed in range(3):
+        TA.test_zero_summaries_one_window_is_dense_causal(seed)
+        TA.test_zero_keys_give_mean_of_visible_values_one_hot(seed)
+        TA.test_sequential_equals_masked_parallel(seed)
+    TA.test_window_attention_matches_brute_force_with_cache()
+    TA.test_rows_sum_to_one_and_respect_mask()
+    TA.test_constant_values_and_first_token()
+    TA.test_discarded_ordinary_kv_is_invisible_but_summaries_are_not()
+    TA.test_strict_causality()
+    TA.test_grouped_kv_heads_equal_repeated_heads()
+    TA.test_scale_enters_only_through_scores()
+    TA.test_compaction_keeps_summary_rows_in_order(0)
+
+
+def _decode_pins():
+    TD.test_decode_from_empty_equals_prefill(37, 10, 3)
+    TD.test_decode_from_empty_equals_prefill(25, 7, 7)
+    TD.test_decode_mid_window_start_equals_prefill(11)
+    TD.test_cache_growth_and_window_reset()
+
+
+ATTENTION_MUTATIONS = [
+    ("strict causal mask", "((j - n_cache) <= i)", "((j - n_cache) < i)"),
+    ("last cache row hidden", "return (j < n_cache) | ((j - n_cache) <= i)",
+     "return (j < n_cache - 1) | ((j >= n_cache) & ((j - n_cache) <= i))"),
+    ("window sees its future", "((j - n_cache) <= i)", "((j - n_cache) <= i + 1)"),
+    ("scale dropped", "s = scale * (q @ keys.T)", "s = (q @ keys.T)"),
+    ("no max shift in lse", "lse = (m + np.log(l))[:, 0]", "lse = np.log(l)[:, 0]"),
+    ("values of the wrong rows", "o = p @ values", "o = p @ values[::-1]"),
+    ("kv head of the wrong group", "g = h // (H // Hkv)\n        keys", "g = h % Hkv\n        keys"),
+    ("ordinary rows kept", "keep = np.nonzero(layout[\"tok_kind\"][t0:t1] == SUMMARY)[0] + t0",
+     "keep = np.arange(t0, t1)"),
+    ("masked-parallel without summaries", "| is_sum[None, :])", ")"),
+    ("cache offset off by one", "first:first + int(layout[\"win_cache_off\"][w])]",
+     "first:first + int(layout[\"win_cache_off\"][w]) + 1]"),
+]
+
+LAYOUT_MUTATIONS = [
+    ("summary before its k-mer", "closes_kmer = since_summary == k", "closes_kmer = since_summary == 1"),
+    ("partial k-mer without summary", "closes_window = i == stop - 1 and since_summary > 0",
+     "closes_window = False"),
+    ("cache rows not carried", "cache_rows += j\n", "cache_rows += 0\n"),
+    ("window one base short", "stop = min(start + W, L)", "stop = min(start + W - 1, L)"),
+    ("kmer row of next summary", "emit(BASE, g_base0 + i, cache_rows + j if k > 0 else -1)",
+     "emit(BASE, g_base0 + i, cache_rows + j + 1 if k > 0 else -1)"),
+]
+
+DECODE_MUTATIONS = [
+    ("no summary for partial window", "(self.bases_in_window == W and self.bases_in_kmer > 0)", "False"),
+    ("window never reset", "self.win_k, self.win_v = [], []", "pass"),
+    ("summary into window buffer", "self.cache_k.append(np.asarray(k_new))",
+     "self.win_k.append(np.asarray(k_new))"),
+]
+
+
+def _expect_caught(monkeypatch, pins, patches):
+    for mod_obj, attr, value in patches:
+        monkeypatch.setattr(mod_obj, attr, value)
+    with pytest.raises((AssertionError, ValueError, IndexError)):
+        pins()
+
+
+@pytest.mark.parametrize("name,old,new", ATTENTION_MUTATIONS, ids=[m[0] for m in ATTENTION_MUTATIONS])
+def test_attention_mutations_are_caught(monkeypatch, name, old, new):
+    mut = _mutant(oracle.attention, old, new)
+    _expect_caught(monkeypatch, _attention_pins, [(TA, "A", mut)])
+
+
+@pytest.mark.parametrize("name,old,new", LAYOUT_MUTATIONS, ids=[m[0] for m in LAYOUT_MUTATIONS])
+def test_layout_mutations_are_caught(monkeypatch, name, old, new):
+    mut = _mutant(oracle.layout, old, new)
+    _expect_caught(monkeypatch, _layout_pins, [(TL, "build_layout", mut.build_layout)])
+
+
+@pytest.mark.parametrize("name,old,new", DECODE_MUTATIONS, ids=[m[0] for m in DECODE_MUTATIONS])
+def test_decode_mutations_are_caught(monkeypatch, name, old, new):
+    mut = _mutant(oracle.decode, old, new)
+    _expect_caught(monkeypatch, _decode_pins, [(TD, "DecodeSequence", mut.DecodeSequence)])
+
+
+def test_unmutated_pins_pass():
+    _layout_pins()
+    _attention_pins()
+    _decode_pins()
