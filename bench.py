@@ -1,0 +1,399 @@
+"""Benchmark of the FOCUS hot path on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1]
+
+One step = one pass of the whole prefill hot path over a 1 Mb sequence
+(1 000 windows of 1 000 nt, a summary token every 100 nt, 32 heads x 128, bf16):
+focus_layout, then focus_compact_kv over every window (10 000 retained rows),
+then focus_window_attn over every window in one masked-parallel launch.
+Inputs (Q, K, V) are resident in HBM before timing starts.  `value` is input
+nucleotides per second over the timed steps.
+
+Also reported on the same JSON line:
+  roofline      the attention kernel against the bf16 MFMA peak, timed with
+                HIP events on the stream it runs on; `traffic` from the
+                committed rocprofv3 counter summary when it matches the current
+                kernel source, else null
+  cpu_baseline  the float64 oracle on a bounded sample of the same workload
+                (whole windows, all heads), extrapolated by visible pairs
+  secondary     compaction and decode (batch 16 at ~1 Mb) HBM rates, the dense
+                32 kb causal point, and streaming (one window per call) prefill
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "window-attention tokens/s at 1 Mb context; % MFMA peak (prefill), % HBM BW (decode)"
+PEAK_BF16_FLOPS = 2.5e15      # MI355X dense bf16 MFMA
+PEAK_HBM = 8.0e12             # MI355X HBM3E bytes/s
+ATTN_SOURCES = ["paper_2511_14694_amd/csrc/window_attn.hip", "paper_2511_14694_amd/csrc/common.h"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_window_attn_prefill_1mb.json")
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def source_hash(paths):
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def visible_pairs(win_ntok, win_cache_off):
+    """Query-key pairs the C(t) mask admits: every window query sees its C_w
+    cache rows and the i + 1 window rows up to itself."""
+    T = win_ntok.astype(np.int64)
+    C = win_cache_off.astype(np.int64)
+    return int((T * C + T * (T + 1) // 2).sum())
+
+
+class Timer:
+    """HIP events on the current stream (the one every library call uses)."""
+
+    def __init__(self, torch):
+        self.torch = torch
+        self.marks = {}
+
+    def span(self, name):
+        torch = self.torch
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        self.marks.setdefault(name, []).append((s, e))
+        return s, e
+
+    def mean_ms(self, name):
+        xs = [s.elapsed_time(e) for s, e in self.marks.get(name, [])]
+        return float(np.mean(xs)) if xs else float("nan")
+
+
+def prefill_setup(torch, F, fw, w):
+    dev = torch.device("cuda:0")
+    seq = [w.seq_nt] * w.batch
+    kmer = fw.kmer_draw(w)
+    totals = F.focus_layout_plan(seq, w.window_nt, kmer)
+    seq_d = torch.as_tensor(np.asarray(seq, np.int64), device=dev)
+    kmer_d = torch.as_tensor(kmer, device=dev)
+    lay = F.focus_layout(totals, seq_d, w.window_nt, kmer_d, device=dev)
+    n = totals.n_tokens
+    q, k, v = fw.qkv(n, w, device=dev)
+    cap = max(totals.max_cache_per_seq, 1)
+    td = q.dtype
+    ck = torch.empty(w.batch, cap, w.kv_heads, w.head_dim, dtype=td, device=dev)
+    cv = torch.empty_like(ck)
+    clen = torch.zeros(w.batch, dtype=torch.int32, device=dev)
+    o = torch.empty_like(q)
+    lse = torch.empty(n, w.heads, dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+    return dict(seq_d=seq_d, kmer_d=kmer_d, totals=totals, lay=lay, q=q, k=k, v=v, ck=ck, cv=cv,
+                clen=clen, o=o, lse=lse, w=w)
+
+
+def prefill_step(torch, F, s, timer=None):
+    w = s["w"]
+    t = timer.span if timer else None
+    if t:
+        a = t("layout")
+        a[0].record()
+    F.focus_layout(s["totals"], s["seq_d"], w.window_nt, s["kmer_d"], out=s["lay"])
+    if t:
+        a[1].record()
+        a = t("compact")
+        a[0].record()
+    s["clen"].zero_()
+    F.focus_compact_kv(s["lay"], s["k"], s["v"], s["ck"], s["cv"], s["clen"])
+    if t:
+        a[1].record()
+        a = t("attn")
+        a[0].record()
+    F.focus_window_attn(s["lay"], s["q"], s["k"], s["v"], s["ck"], s["cv"], o=s["o"], lse=s["lse"])
+    if t:
+        a[1].record()
+
+
+def cpu_baseline(torch, s, budget_s=20.0):
+    """The oracle, as it is, on whole windows of the same workload (all heads):
+    the last window first, then earlier ones, until the time budget is used.
+    The full-workload time is extrapolated by the visible-pair ratio."""
+    from oracle import attention as A
+    from oracle.layout import build_layout
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    w = s["w"]
+    t_layout0 = time.perf_counter()
+    ref = build_layout([w.seq_nt] * w.batch, w.window_nt, fw_kmer(w))
+    t_layout = time.perf_counter() - t_layout0
+    nw = ref["n_windows"]
+    order = [nw - 1, nw // 2, nw // 4, 3 * nw // 4, 1]
+    done, pairs, t_attn = [], 0, 0.0
+    for wi in order:
+        t0, T = int(ref["win_tok_off"][wi]), int(ref["win_ntok"][wi])
+        idx = A.cache_token_indices(ref, wi)
+        f64 = lambda x: x.float().cpu().numpy().astype(np.float64)  # noqa: E731
+        q, k, v = f64(s["q"][t0:t0 + T]), f64(s["k"][t0:t0 + T]), f64(s["v"][t0:t0 + T])
+        ti = torch.as_tensor(idx, device=s["k"].device)
+        ck, cv = f64(s["k"][ti]), f64(s["v"][ti])
+        c0 = time.perf_counter()
+        A.window_attention(q, k, v, ck, cv)
+        t_attn += time.perf_counter() - c0
+        done.append(wi)
+        pairs += T * len(idx) + T * (T + 1) // 2
+        if t_attn > budget_s:
+            break
+    total_pairs = visible_pairs(ref["win_ntok"], ref["win_cache_off"])
+    t_full = t_attn * total_pairs / pairs + t_layout
+    return {"value": w.seq_nt * w.batch / t_full, "unit": "nt/s", "cores": int(cores), "kind": "oracle",
+            "sample": (f"oracle window attention on windows {done} (all {w.heads} heads, "
+                       f"{pairs:,} of {total_pairs:,} visible pairs per head) in {t_attn:.1f} s, "
+                       f"plus the full oracle layout walk ({t_layout:.1f} s); full-workload time "
+                       f"extrapolated by the visible-pair ratio to {t_full:.0f} s")}
+
+
+def fw_kmer(w):
+    import focus_workloads as fw
+    return fw.kmer_draw(w)
+
+
+def traffic_entry():
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    rec = json.load(open(TRAFFIC_FILE))
+    if rec.get("source_hash") != source_hash(ATTN_SOURCES):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def secondary_compaction(torch, F, s, timer, reps=10):
+    """Bulk compaction at 1 Mb with the 256 MB last-level cache flushed first."""
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda:0")
+    for _ in range(reps):
+        flush.fill_(1)
+        a = timer.span("compact_cold")
+        a[0].record()
+        F.focus_compact_kv(s["lay"], s["k"], s["v"], s["ck"], s["cv"], s["clen"])
+        a[1].record()
+    torch.cuda.synchronize()
+    w = s["w"]
+    row = w.kv_heads * w.head_dim * 2
+    nbytes = s["totals"].n_summaries * row * 2 * 2          # K and V, read + write
+    ms = timer.mean_ms("compact_cold")
+    return {"rows": s["totals"].n_summaries, "bytes": nbytes, "ms": ms,
+            "GBps": nbytes / ms / 1e6, "frac_hbm": nbytes / (ms * 1e-3) / PEAK_HBM}
+
+
+def secondary_decode(torch, F, fw, steps=None):
+    """Batch-16 decode at ~1 Mb: 10 000 cached summaries plus a partial window."""
+    from paper_2511_14694_amd import schedule
+    w = fw.WORKLOADS["decode_b16_1mb"]
+    dev = torch.device("cuda:0")
+    steps = steps or w.decode_steps
+    B, H, Hkv, D = w.batch, w.heads, w.kv_heads, w.head_dim
+    totals = F.focus_layout_plan([w.window_nt], w.window_nt, None, w.kmer)
+    lay1 = F.focus_layout(totals, [w.window_nt], w.window_nt, None, w.kmer, device=dev)
+    kinds_win = lay1["tok_kind"].cpu().numpy()
+    starts = fw.decode_positions(w)
+    n0 = [schedule.initial_lengths(kinds_win, int(p)) for p in starts]
+    cap_c = w.decode_cache_rows + 2 * (-(-w.window_nt // w.kmer)) + 8
+    seed = fw.seed_for(w.index, "cache_k")
+    cache_k = fw.randn((B, cap_c, Hkv, D), w.dtype, seed + 1, dev)
+    cache_v = fw.randn((B, cap_c, Hkv, D), w.dtype, seed + 2, dev)
+    win_k = fw.randn((B, w.window_nt, Hkv, D), w.dtype, seed + 3, dev)
+    win_v = fw.randn((B, w.window_nt, Hkv, D), w.dtype, seed + 4, dev)
+    sq = fw.randn((steps, B, H, D), w.dtype, seed + 5, dev)
+    sk = fw.randn((steps, B, Hkv, D), w.dtype, seed + 6, dev)
+    sv = fw.randn((steps, B, Hkv, D), w.dtype, seed + 7, dev)
+    cache_len = torch.tensor([w.decode_cache_rows + a for a, _ in n0], dtype=torch.int32, device=dev)
+    win_len = torch.tensor([b for _, b in n0], dtype=torch.int32, device=dev)
+    kinds = torch.as_tensor(np.stack([schedule.step_kinds(kinds_win, int(p), steps) for p in starts], 1),
+                            device=dev)
+    # keys read per step, for the algorithmic byte count (host-side replay of the lengths)
+    kh = kinds.cpu().numpy()
+    cl = np.array([w.decode_cache_rows + a for a, _ in n0], np.int64)
+    wl = np.array([b for _, b in n0], np.int64)
+    keys = 0
+    for i in range(steps):
+        summ = (kh[i] & 1) > 0
+        cl += summ
+        wl += ~summ
+        keys += int((cl + wl).sum())
+        wl[(kh[i] & 2) > 0] = 0
+    row = Hkv * D * 2
+    nbytes = keys * row * 2 + steps * B * (2 * H * D * 2 + 2 * row + H * 4)
+    o = torch.empty(B, H, D, dtype=torch.bfloat16, device=dev)
+    lse = torch.empty(B, H, dtype=torch.float32, device=dev)
+    ws = torch.empty(F.focus_decode_workspace(sq[0], sk[0], cache_k, win_k), dtype=torch.uint8, device=dev)
+    # warm-up on copies of the state, then the timed run from the initial state
+    st = [cache_len.clone(), win_len.clone()]
+    for i in range(min(20, steps)):
+        F.focus_decode_step(sq[i], sk[i], sv[i], kinds[i], cache_k, cache_v, st[0], win_k, win_v, st[1],
+                            o=o, lse=lse, workspace=ws)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(steps):
+        F.focus_decode_step(sq[i], sk[i], sv[i], kinds[i], cache_k, cache_v, cache_len, win_k, win_v, win_len,
+                            o=o, lse=lse, workspace=ws)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    return {"workload": "decode_b16_1mb: batch 16, 32 x 128 bf16, 10 000 cached summaries + partial window, "
+                        f"{steps} steps", "tokens_per_s": B * steps / (ms * 1e-3), "ms_per_step": ms / steps,
+            "bytes_per_step": nbytes / steps, "GBps": nbytes / ms / 1e6,
+            "frac_hbm": nbytes / (ms * 1e-3) / PEAK_HBM}
+
+
+def secondary_dense(torch, F, fw, reps=3):
+    w = fw.WORKLOADS["dense_32kb"]
+    s = prefill_setup(torch, F, fw, w)
+    F.focus_window_attn(s["lay"], s["q"], s["k"], s["v"], s["ck"], s["cv"], o=s["o"], lse=s["lse"])
+    timer = Timer(torch)
+    for _ in range(reps):
+        a = timer.span("dense")
+        a[0].record()
+        F.focus_window_attn(s["lay"], s["q"], s["k"], s["v"], s["ck"], s["cv"], o=s["o"], lse=s["lse"])
+        a[1].record()
+    torch.cuda.synchronize()
+    ms = timer.mean_ms("dense")
+    n = w.seq_nt
+    flops = 4 * w.head_dim * w.heads * (n * (n + 1) // 2)
+    return {"workload": "dense_32kb: one 32 000-token causal window, no summaries, 32 x 128 bf16",
+            "ms": ms, "tflops": flops / ms / 1e9, "frac_mfma": flops / (ms * 1e-3) / PEAK_BF16_FLOPS,
+            "dense_1mb_extrapolated_s": ms * 1e-3 * (1e6 / n) ** 2}
+
+
+def secondary_streaming(torch, F, s, n_windows=200):
+    """Streaming prefill: one window per call (last n_windows windows)."""
+    lay = s["lay"]
+    nw = lay.totals.n_windows
+    ids = [torch.tensor([w_], dtype=torch.int32, device="cuda:0") for w_ in range(nw - n_windows, nw)]
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in ids:
+        F.focus_window_attn(lay, s["q"], s["k"], s["v"], s["ck"], s["cv"], o=s["o"], lse=s["lse"], win_ids=i)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    return {"windows": n_windows, "ms_per_window": ms / n_windows,
+            "note": "one launch per window (the last windows, largest caches)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="prefill_1mb")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-secondary", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run one 1 GiB device copy (HBM counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: the FOCUS hot path here runs on a single MI355X and "
+              f"has no multi-GPU mode (asked for --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import focus_workloads as fw
+    import paper_2511_14694_amd as F
+    F._abi.lib()
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+
+    w = fw.WORKLOADS[args.workload]
+    log(f"setup {w.name}")
+    s = prefill_setup(torch, F, fw, w)
+    if args.copy_calibration:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda:0").fill_(3)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+    for i in range(args.warmup):
+        prefill_step(torch, F, s)
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps)")
+    timer = Timer(torch)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for i in range(args.steps):
+        prefill_step(torch, F, s, timer)
+    e1.record()
+    torch.cuda.synchronize()
+    total_ms = e0.elapsed_time(e1)
+    ms_step = total_ms / max(args.steps, 1)
+    log(f"timed {args.steps} steps: {ms_step:.3f} ms/step")
+
+    lay_np = {k: s["lay"][k].cpu().numpy() for k in ("win_ntok", "win_cache_off")}
+    pairs = visible_pairs(lay_np["win_ntok"], lay_np["win_cache_off"])
+    flops = 4 * w.head_dim * w.heads * pairs
+    attn_ms = timer.mean_ms("attn")
+    traffic = traffic_entry()
+    nt = w.seq_nt * w.batch
+    result = {
+        "metric": METRIC,
+        "value": nt / (ms_step * 1e-3),
+        "unit": "nt/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: batch {w.batch} x {w.seq_nt:,} nt, windows of {w.window_nt} nt, "
+                               f"one summary token per {w.kmer} nt, {w.heads} heads x {w.head_dim} "
+                               f"{w.dtype}; step = layout + compaction + masked-parallel window attention",
+                   "augmented_tokens": s["totals"].n_tokens, "visible_pairs_per_head": pairs},
+        "roofline": {"bound": "mfma", "achieved": flops / (attn_ms * 1e-3) / 1e12,
+                     "peak": PEAK_BF16_FLOPS / 1e12, "unit": "TFLOP/s",
+                     "frac": flops / (attn_ms * 1e-3) / PEAK_BF16_FLOPS, "traffic": traffic,
+                     "kernel": "attn_bf16<128> (focus_window_attn)", "flops_per_launch": flops,
+                     "avg_launch_ms": attn_ms},
+        "kernel_ms": {"layout": timer.mean_ms("layout"), "compact": timer.mean_ms("compact"),
+                      "attn": attn_ms},
+        "augmented_tokens_per_s": s["totals"].n_tokens / (ms_step * 1e-3),
+    }
+    if not args.no_secondary:
+        log("secondary: compaction")
+        sec = {"compaction_1mb": secondary_compaction(torch, F, s, timer)}
+        log("secondary: streaming")
+        sec["streaming_1mb"] = secondary_streaming(torch, F, s)
+        if not args.no_cpu_baseline:
+            log("cpu baseline (oracle)")
+            result["cpu_baseline"] = cpu_baseline(torch, s, args.cpu_budget)
+        del s
+        torch.cuda.empty_cache()
+        log("secondary: decode")
+        sec["decode_b16_1mb"] = secondary_decode(torch, F, fw)
+        torch.cuda.empty_cache()
+        log("secondary: dense 32 kb")
+        sec["dense_32kb"] = secondary_dense(torch, F, fw)
+        result["secondary"] = sec
+    elif not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(torch, s, args.cpu_budget)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

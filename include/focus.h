@@ -1,0 +1,330 @@
+/*
+ * focus.h -- C interface of the FOCUS hot path for AMD MI355X (CDNA4, gfx950).
+ *
+ * FOCUS (arXiv 2511.14694) inserts one summary token after every k bases of a
+ * DNA sequence, processes the sequence in base-domain windows, and keeps only
+ * the summary tokens' key/value rows across windows.  This library implements
+ * the per-layer hot path of that scheme:
+ *
+ *   focus_layout_plan / focus_layout   summary-token layout and index metadata
+ *   focus_compact_kv                   append summary K/V rows to the cache
+ *   focus_window_attn                  window attention over [cache ; window]
+ *   focus_decode_step                  one-token decode over [cache ; window]
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * Memory.  Pointers marked [device] are HIP device pointers owned by the
+ *   caller; [host] pointers are ordinary host memory.  The library never
+ *   allocates, frees or keeps a pointer after a call returns.  Tensors are
+ *   row-major with head_dim contiguous and 16-byte aligned base pointers:
+ *     token tensors   [rows, heads, head_dim]       ("THD")
+ *     caches          [batch, capacity, kv_heads, head_dim]
+ * Types.  FOCUS_BF16 tensors hold bfloat16, FOCUS_F32 tensors float32; one
+ *   call uses one dtype for q, k, v, caches and o.  Scores, softmax and
+ *   accumulation are float32; o is rounded to the tensor dtype (nearest-even);
+ *   lse is float32 natural-log.
+ * Execution.  Every device-side call only enqueues kernels on `stream` (a
+ *   hipStream_t passed as void*; NULL = the null stream) and never
+ *   synchronises.  Calls are re-entrant; the library holds no state.
+ * Errors.  Every call returns a focus_status.  Problems visible on the host
+ *   (NULL or misaligned pointers, inconsistent sizes, unsupported shapes, a
+ *   short workspace) are reported before anything is enqueued, so nothing is
+ *   written.  Problems only the device can see (a row index outside a buffer, a
+ *   cache at capacity, layout totals that differ from the plan) skip the
+ *   affected rows and OR a FOCUS_ERR_* bit into the optional [device] `err`
+ *   word; no kernel ever writes outside the buffers described to it.
+ * Indexing (0-based).  Windows, augmented tokens and summaries of all
+ *   sequences of a batch are numbered globally, sequence after sequence
+ *   ("global window / token / summary index"); bases of all sequences are
+ *   concatenated ("global base index"); a cache row is counted inside its own
+ *   sequence.
+ */
+#ifndef FOCUS_H
+#define FOCUS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FOCUS_ABI_VERSION 1
+
+typedef int32_t focus_status;
+enum {
+  FOCUS_OK = 0,
+  FOCUS_E_NULL = 1,        /* a required pointer is NULL                        */
+  FOCUS_E_ARG = 2,         /* a value out of range, or a misaligned pointer     */
+  FOCUS_E_SHAPE = 3,       /* sizes inconsistent with each other                */
+  FOCUS_E_DTYPE = 4,       /* unknown dtype                                     */
+  FOCUS_E_UNSUPPORTED = 5, /* well-formed request this build does not implement */
+  FOCUS_E_WORKSPACE = 6,   /* workspace missing or too small                    */
+  FOCUS_E_CAPACITY = 7,    /* a cache is too small for the planned rows         */
+  FOCUS_E_HIP = 8          /* the HIP runtime refused a launch                  */
+};
+
+typedef enum { FOCUS_BF16 = 0, FOCUS_F32 = 1 } focus_dtype;
+
+/* Visibility rule of focus_window_attn.
+ * FOCUS_MASK_CT: the set C(t) of Appendix A.1 ("Objective and visibility"):
+ *   a token sees every earlier-or-equal token of its own window and every
+ *   retained summary of the earlier windows of its sequence.
+ * FOCUS_MASK_KMER_LOCAL: the stricter Section 3.2 rule (a base sees only its own
+ *   k-mer and earlier summaries of its window); returns FOCUS_E_UNSUPPORTED. */
+typedef enum { FOCUS_MASK_CT = 0, FOCUS_MASK_KMER_LOCAL = 1 } focus_mask;
+
+/* tok_kind values */
+enum { FOCUS_TOK_BASE = 0, FOCUS_TOK_SUMMARY = 1 };
+/* focus_decode_desc.kind bits */
+enum { FOCUS_STEP_SUMMARY = 1, FOCUS_STEP_WINDOW_END = 2 };
+/* bits of the device error word */
+enum { FOCUS_ERR_CAPACITY = 1, FOCUS_ERR_BOUNDS = 2, FOCUS_ERR_PLAN = 4 };
+
+typedef void* focus_stream_t;   /* a hipStream_t */
+
+int32_t focus_abi_version(void);
+const char* focus_status_str(focus_status s);
+/* sizeof of the descriptor structs below, in declaration order
+ * (0 totals, 1 layout, 2 compact, 3 attn, 4 decode); -1 otherwise.
+ * Lets a binding check its mirror of the structs. */
+int64_t focus_struct_size(int32_t which);
+
+/* ------------------------------------------------------------------------ */
+/* Layout                                                                    */
+/* ------------------------------------------------------------------------ */
+
+/* Totals of a layout, computed on the host by focus_layout_plan. */
+typedef struct {
+  int64_t n_windows;            /* sum_b ceil(L_b / W)                       */
+  int64_t n_tokens;             /* augmented tokens: bases + summaries       */
+  int64_t n_summaries;          /* sum_w B_w                                 */
+  int64_t max_window_tokens;    /* max_w T_w, T_w = n_w + B_w                */
+  int64_t max_window_summaries; /* max_w B_w                                 */
+  int64_t max_cache_per_seq;    /* max_b sum_{w in b} B_w (cache rows needed) */
+  int64_t max_window_cache;     /* max_w C_w (cache rows a window attends to) */
+} focus_layout_totals;
+
+/* Summary-token layout totals (Appendix A: windows I_w = [(w-1)W+1, wW] clipped
+ * to [1, L], ceil(L/W) per sequence, B_w = ceil(|I_w| / k_w) summaries each;
+ * Section 3.2: one summary after every k bases, a trailing partial k-mer
+ * included).
+ *   batch      number of sequences, >= 0
+ *   seq_nt     [host] [batch] bases per sequence, each >= 0
+ *   window_nt  W, bases per window, >= 1
+ *   kmer       [host] [n_windows] cadence k_w per global window, or NULL to
+ *              use kmer_uniform for all; k_w = 0 means no summary tokens
+ *   out        [host] receives the totals
+ * O(number of windows) host work.  Errors: E_NULL, E_ARG. */
+focus_status focus_layout_plan(int32_t batch, const int64_t* seq_nt, int32_t window_nt,
+                               const int32_t* kmer, int32_t kmer_uniform,
+                               focus_layout_totals* out);
+
+/* Everything focus_layout reads and writes.  All arrays [device].
+ * Per window w (global index): the window belongs to sequence win_seq[w], holds
+ * n_w = win_nt[w] bases and B_w = win_nsum[w] summaries, T_w = win_ntok[w]
+ * augmented tokens starting at global token win_tok_off[w] and global base
+ * win_base_off[w]; its first summary is global summary win_sum_off[w]; it sees
+ * cache rows [0, C_w) with C_w = win_cache_off[w].
+ * Per token t (global index), in window order [k-mer bases, summary, ...]:
+ * tok_kind[t] (FOCUS_TOK_*), tok_pos[t] = position in its sequence's augmented
+ * stream, tok_win[t] = window, tok_base[t] = global base index or -1 for a
+ * summary, tok_kmer[t] = cache row of the summary closing its k-mer (-1 when
+ * k_w = 0), token_ids[t] = bases[tok_base[t]] or summary_token_id.
+ * Per summary s: sum_tok[s] = its global token index.
+ * cu_*[b] = first global window / token / summary of sequence b; cu_*[batch] =
+ * the total. */
+typedef struct {
+  focus_layout_totals totals;   /* from focus_layout_plan on the same inputs */
+  int32_t batch;
+  int32_t window_nt;
+  int32_t kmer_uniform;         /* cadence when kmer == NULL                 */
+  int32_t summary_token_id;     /* token id written at summary positions    */
+  const int64_t* seq_nt;        /* [batch]                                   */
+  const int32_t* kmer;          /* [n_windows] or NULL                       */
+  const uint8_t* bases;         /* [sum seq_nt] base bytes, or NULL           */
+  int64_t* cu_windows;          /* [batch + 1]                               */
+  int64_t* cu_tokens;           /* [batch + 1]                               */
+  int64_t* cu_summaries;        /* [batch + 1]                               */
+  int32_t* win_seq;             /* [n_windows]                               */
+  int32_t* win_nt;
+  int32_t* win_nsum;
+  int32_t* win_ntok;
+  int32_t* win_cache_off;
+  int64_t* win_tok_off;
+  int64_t* win_sum_off;
+  int64_t* win_base_off;
+  int32_t* tok_pos;             /* [n_tokens]                                */
+  int32_t* tok_kmer;
+  int32_t* tok_win;
+  uint8_t* tok_kind;
+  int64_t* tok_base;
+  int64_t* sum_tok;             /* [n_summaries]                             */
+  int32_t* token_ids;           /* [n_tokens], written only if bases != NULL */
+  int32_t* err;                 /* optional error word                       */
+} focus_layout_desc;
+
+/* Fill every layout array (definitions above).  The result is bit-exact: it is
+ * pure integer work.  Device check: if the totals the device finds differ from
+ * d->totals, FOCUS_ERR_PLAN is raised and nothing beyond the planned sizes is
+ * written.  Errors: E_NULL, E_ARG, E_SHAPE, E_HIP. */
+focus_status focus_layout(const focus_layout_desc* d, focus_stream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Compaction                                                                */
+/* ------------------------------------------------------------------------ */
+
+/* Retained-KV compaction (Appendix A "KV compression and budget", A.2): after
+ * window w, the K/V rows of its B_w summary tokens are appended to its
+ * sequence's cache, at rows [C_w, C_w + B_w); ordinary rows are not copied.
+ * The shared boundary summary is the last row window w writes and is stored
+ * once.  The copy is bit-exact. */
+typedef struct {
+  focus_layout_totals totals;   /* of the layout the arrays below belong to  */
+  int32_t dtype;                /* focus_dtype of k, v, cache_k, cache_v     */
+  int32_t n_kv_heads;
+  int32_t head_dim;             /* 64 or 128                                 */
+  int32_t batch;
+  int64_t n_win;                /* entries of win_ids (ignored if NULL)      */
+  const int32_t* win_ids;       /* [device] global windows to compact, or
+                                   NULL for every window of the layout       */
+  const int32_t* win_seq;       /* [device] layout arrays                    */
+  const int32_t* win_nsum;
+  const int32_t* win_cache_off;
+  const int64_t* win_sum_off;
+  const int64_t* sum_tok;
+  const void* k;                /* [kv_rows, n_kv_heads, head_dim]: row r is  */
+  const void* v;                /*   global token kv_tok_base + r             */
+  int64_t kv_tok_base;
+  int64_t kv_rows;
+  void* cache_k;                /* [batch, cache_cap, n_kv_heads, head_dim]  */
+  void* cache_v;
+  int64_t cache_cap;
+  int32_t* cache_len;           /* [device][batch] or NULL: raised (never
+                                   lowered) to C_w + B_w of each listed window */
+  int32_t* err;                 /* optional error word                       */
+} focus_compact_desc;
+
+/* Errors: E_NULL, E_ARG, E_DTYPE, E_SHAPE, E_UNSUPPORTED, E_CAPACITY (the
+ * plan's max_cache_per_seq exceeds cache_cap), E_HIP.  A summary row outside
+ * [0, kv_rows) or a cache row >= cache_cap is skipped on the device with
+ * FOCUS_ERR_BOUNDS / FOCUS_ERR_CAPACITY. */
+focus_status focus_compact_kv(const focus_compact_desc* d, focus_stream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Window attention (prefill)                                                */
+/* ------------------------------------------------------------------------ */
+
+/* For every listed window w of sequence b, every head h and every window query
+ * row i in [0, T_w) (global token t = win_tok_off[w] + i):
+ *     keys     = [cache_k[b, 0:C_w, g] ; k[window rows, g]],  g = h / (H / H_kv)
+ *     visible  = every cache row, and window rows u <= i      (FOCUS_MASK_CT)
+ *     o[t, h]  = softmax(scale * q[t, h] . keys^T over visible) . values
+ *     lse[t,h] = log sum_visible exp(scale * q[t, h] . key)
+ * (Appendix A eq. focus-attn with the visibility set C(t) of A.1.)  The cache
+ * rows [0, C_w) must hold the summaries of the earlier windows, as
+ * focus_compact_kv leaves them; windows may be listed in any order and mixed
+ * across sequences (the masked-parallel form of A.1), or one at a time
+ * (streaming, A.2).  Windows listed first are started first: list the ones
+ * with the largest C_w + T_w first.
+ *   softmax_scale <= 0 selects 1/sqrt(head_dim).
+ *   Supported: head_dim 64 or 128, bf16 or f32, n_heads a multiple of n_kv_heads.
+ */
+typedef struct {
+  focus_layout_totals totals;
+  int32_t dtype;
+  int32_t n_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  float softmax_scale;
+  int32_t mask;                 /* focus_mask                                */
+  int32_t batch;
+  int32_t reserved;
+  int64_t n_win;                /* entries of win_ids (ignored if NULL)      */
+  const int32_t* win_ids;       /* [device] or NULL = all windows, in the
+                                   order last window first                   */
+  const int32_t* win_seq;       /* [device] layout arrays                    */
+  const int32_t* win_ntok;
+  const int32_t* win_cache_off;
+  const int64_t* win_tok_off;
+  const void* q;                /* [qkv_rows, n_heads, head_dim]             */
+  const void* k;                /* [qkv_rows, n_kv_heads, head_dim]          */
+  const void* v;                /*   row r = global token qkv_tok_base + r   */
+  int64_t qkv_tok_base;
+  int64_t qkv_rows;
+  const void* cache_k;          /* [batch, cache_cap, n_kv_heads, head_dim]  */
+  const void* cache_v;
+  int64_t cache_cap;
+  void* o;                      /* [qkv_rows, n_heads, head_dim], dtype      */
+  float* lse;                   /* [qkv_rows, n_heads] float32, or NULL      */
+  void* workspace;              /* may be NULL if the size query returns 0   */
+  size_t workspace_bytes;
+  int32_t* err;
+} focus_attn_desc;
+
+/* Workspace bytes focus_window_attn needs for this descriptor (0 today). */
+size_t focus_window_attn_workspace(const focus_attn_desc* d);
+/* Errors: E_NULL, E_ARG, E_DTYPE, E_SHAPE, E_UNSUPPORTED, E_WORKSPACE,
+ * E_CAPACITY (plan's max_window_cache > cache_cap), E_HIP.  A window whose rows
+ * fall outside the buffers is skipped with FOCUS_ERR_BOUNDS. */
+focus_status focus_window_attn(const focus_attn_desc* d, focus_stream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Decode                                                                    */
+/* ------------------------------------------------------------------------ */
+
+/* One autoregressive step for every sequence b of a batch (Appendix A.2,
+ * streaming inference with the retained summary cache):
+ *   1. append (k_new[b], v_new[b]) to the cache at row cache_len[b] if
+ *      kind[b] & FOCUS_STEP_SUMMARY, else to the window buffer at row
+ *      win_len[b]; bump that length;
+ *   2. o[b, h] = softmax(scale * q[b, h] . [cache[0:cache_len] ;
+ *      win[0:win_len]]^T) . values, every row visible; lse likewise;
+ *   3. if kind[b] & FOCUS_STEP_WINDOW_END, set win_len[b] = 0 afterwards.
+ * The caller derives kind from the layout (a summary every k bases, the last
+ * summary of a window ends it).  Keys are split into chunks of split_keys rows
+ * processed in parallel and merged by log-sum-exp; results do not depend on
+ * the split beyond float32 rounding, and are deterministic for a fixed split.
+ * All state lives in device memory, so steps can be enqueued back to back
+ * without host synchronisation.
+ */
+typedef struct {
+  int32_t dtype;
+  int32_t batch;
+  int32_t n_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;             /* 64 or 128                                 */
+  float softmax_scale;          /* <= 0: 1/sqrt(head_dim)                    */
+  int32_t split_keys;           /* keys per split, multiple of 16; 0 = auto  */
+  int32_t reserved;
+  const void* q;                /* [batch, n_heads, head_dim]                */
+  const void* k_new;            /* [batch, n_kv_heads, head_dim]             */
+  const void* v_new;
+  const uint8_t* kind;          /* [device][batch] FOCUS_STEP_* bits         */
+  void* cache_k;                /* [batch, cache_cap, n_kv_heads, head_dim]  */
+  void* cache_v;
+  int64_t cache_cap;
+  int32_t* cache_len;           /* [device][batch] in/out                    */
+  void* win_k;                  /* [batch, win_cap, n_kv_heads, head_dim]    */
+  void* win_v;
+  int64_t win_cap;
+  int32_t* win_len;             /* [device][batch] in/out                    */
+  void* o;                      /* [batch, n_heads, head_dim]                */
+  float* lse;                   /* [batch, n_heads] or NULL                  */
+  void* workspace;
+  size_t workspace_bytes;
+  int32_t* err;
+} focus_decode_desc;
+
+/* Workspace bytes for the split partials of this descriptor. */
+size_t focus_decode_workspace(const focus_decode_desc* d);
+/* Errors: E_NULL, E_ARG, E_DTYPE, E_SHAPE, E_UNSUPPORTED, E_WORKSPACE, E_HIP.
+ * An append into a full cache or window buffer is skipped with
+ * FOCUS_ERR_CAPACITY (the step still attends over what is there). */
+focus_status focus_decode_step(const focus_decode_desc* d, focus_stream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FOCUS_H */

@@ -66,7 +66,8 @@ def build_layout(seq_nt, window_nt: int, kmer, bases=None, summary_token_id: int
         raise ValueError("negative cadence")
 
     cu_windows, cu_tokens, cu_summaries = [0], [0], [0]
-    win = {name: [] for name in ("seq", "nt", "nsum", "ntok", "tok_off", "cache_off", "sum_off")}
+    win = {name: [] for name in ("seq", "nt", "nsum", "ntok", "tok_off", "cache_off", "sum_off",
+                                 "base_off")}
     tok = {name: [] for name in ("pos", "kind", "base", "kmer", "win")}
     token_ids = []
     sum_tok = []
@@ -88,6 +89,7 @@ def build_layout(seq_nt, window_nt: int, kmer, bases=None, summary_token_id: int
             win["tok_off"].append(g_token)
             win["cache_off"].append(cache_rows)
             win["sum_off"].append(g_summary)
+            win["base_off"].append(g_base0 + start)
 
             since_summary = 0   # bases of the currently open k-mer
             j = 0               # summaries emitted so far in this window
@@ -141,6 +143,7 @@ def build_layout(seq_nt, window_nt: int, kmer, bases=None, summary_token_id: int
         "win_tok_off": np.asarray(win["tok_off"], i64),
         "win_cache_off": np.asarray(win["cache_off"], i32),
         "win_sum_off": np.asarray(win["sum_off"], i64),
+        "win_base_off": np.asarray(win["base_off"], i64),
         "tok_pos": np.asarray(tok["pos"], i32),
         "tok_kind": np.asarray(tok["kind"], np.uint8),
         "tok_base": np.asarray(tok["base"], i64),

@@ -1,0 +1,268 @@
+"""FOCUS hot path for AMD MI355X (gfx950): Python binding of libfocus.so.
+
+A thin layer over the C ABI declared in include/focus.h: each function below
+has the name of the C call it wraps and only marshals arguments (device
+pointers of torch tensors, the current HIP stream, descriptor structs).  Every
+step of the computation runs in the library's HIP kernels; torch provides
+device memory and streams.  There is no CPU fallback: if libfocus.so is missing
+the first call raises.
+
+    totals = focus_layout_plan(seq_nt, window_nt, kmer)          # host
+    lay    = focus_layout(totals, seq_nt, window_nt, kmer)       # device metadata
+    focus_compact_kv(lay, k, v, cache_k, cache_v, cache_len)     # summary K/V -> cache
+    o, lse = focus_window_attn(lay, q, k, v, cache_k, cache_v)   # [cache ; window] attention
+    o, lse = focus_decode_step(q, k_new, v_new, kind, ...)       # one decode step
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+from dataclasses import dataclass, field
+from typing import Dict, Optional
+
+import numpy as np
+import torch
+
+from ._abi import (AttnDesc, CompactDesc, DecodeDesc, FocusError, LayoutDesc, LayoutTotals,
+                   FOCUS_BF16, FOCUS_F32, FOCUS_MASK_CT, FOCUS_MASK_KMER_LOCAL,
+                   FOCUS_TOK_BASE, FOCUS_TOK_SUMMARY, FOCUS_STEP_SUMMARY, FOCUS_STEP_WINDOW_END,
+                   FOCUS_ERR_CAPACITY, FOCUS_ERR_BOUNDS, FOCUS_ERR_PLAN, check, lib)
+
+__all__ = ["focus_layout_plan", "focus_layout", "focus_compact_kv", "focus_window_attn",
+           "focus_window_attn_workspace", "focus_decode_step", "focus_decode_workspace",
+           "focus_abi_version", "Layout", "LayoutTotals", "FocusError",
+           "FOCUS_BF16", "FOCUS_F32", "FOCUS_MASK_CT", "FOCUS_MASK_KMER_LOCAL",
+           "FOCUS_TOK_BASE", "FOCUS_TOK_SUMMARY", "FOCUS_STEP_SUMMARY", "FOCUS_STEP_WINDOW_END",
+           "FOCUS_ERR_CAPACITY", "FOCUS_ERR_BOUNDS", "FOCUS_ERR_PLAN"]
+
+_DTYPES = {torch.bfloat16: FOCUS_BF16, torch.float32: FOCUS_F32}
+
+WINDOW_FIELDS = ("win_seq", "win_nt", "win_nsum", "win_ntok", "win_cache_off",
+                 "win_tok_off", "win_sum_off", "win_base_off")
+TOKEN_FIELDS = ("tok_pos", "tok_kmer", "tok_win", "tok_kind", "tok_base")
+_FIELD_DTYPE = {"cu_windows": torch.int64, "cu_tokens": torch.int64, "cu_summaries": torch.int64,
+                "win_seq": torch.int32, "win_nt": torch.int32, "win_nsum": torch.int32,
+                "win_ntok": torch.int32, "win_cache_off": torch.int32, "win_tok_off": torch.int64,
+                "win_sum_off": torch.int64, "win_base_off": torch.int64, "tok_pos": torch.int32,
+                "tok_kmer": torch.int32, "tok_win": torch.int32, "tok_kind": torch.uint8,
+                "tok_base": torch.int64, "sum_tok": torch.int64, "token_ids": torch.int32}
+
+
+def focus_abi_version() -> int:
+    return lib().focus_abi_version()
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to libfocus must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream, device) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return stream.cuda_stream
+
+
+def _dtype(t) -> int:
+    if t.dtype not in _DTYPES:
+        raise ValueError(f"unsupported dtype {t.dtype}")
+    return _DTYPES[t.dtype]
+
+
+def focus_layout_plan(seq_nt, window_nt: int, kmer=None, kmer_uniform: int = 0) -> LayoutTotals:
+    """Host-side totals of the layout (sizes every device buffer)."""
+    seq = np.ascontiguousarray(np.asarray(seq_nt, dtype=np.int64).reshape(-1))
+    km = None if kmer is None else np.ascontiguousarray(np.asarray(kmer, dtype=np.int32).reshape(-1))
+    out = LayoutTotals()
+    st = lib().focus_layout_plan(len(seq), seq.ctypes.data if len(seq) else None, int(window_nt),
+                                 None if km is None else km.ctypes.data, int(kmer_uniform),
+                                 C.byref(out))
+    check("focus_layout_plan", st)
+    return out
+
+
+@dataclass
+class Layout:
+    """Device-resident layout produced by focus_layout (arrays named as in focus.h)."""
+    totals: LayoutTotals
+    batch: int
+    window_nt: int
+    arrays: Dict[str, torch.Tensor] = field(default_factory=dict)
+
+    def __getitem__(self, name):
+        return self.arrays[name]
+
+    def to_numpy(self) -> Dict[str, np.ndarray]:
+        return {k: v.cpu().numpy() for k, v in self.arrays.items()}
+
+
+def focus_layout(totals: LayoutTotals, seq_nt, window_nt: int, kmer=None, kmer_uniform: int = 0,
+                 bases=None, summary_token_id: int = 0, err=None, device="cuda", stream=None,
+                 out: Optional[Layout] = None) -> Layout:
+    """Fill the layout arrays on the device.  seq_nt / kmer / bases may be host
+    arrays (copied to the device) or device tensors.  `out`: a Layout of the
+    same totals whose arrays are written again instead of allocating new ones."""
+    dev = torch.device(device)
+    seq = torch.as_tensor(np.asarray(seq_nt, dtype=np.int64) if not torch.is_tensor(seq_nt) else seq_nt,
+                          dtype=torch.int64).to(dev).contiguous()
+    km = None
+    if kmer is not None:
+        km = torch.as_tensor(np.asarray(kmer, dtype=np.int32) if not torch.is_tensor(kmer) else kmer,
+                             dtype=torch.int32).to(dev).contiguous()
+    bs = None
+    if bases is not None:
+        bs = torch.as_tensor(np.asarray(bases, dtype=np.uint8) if not torch.is_tensor(bases) else bases,
+                             dtype=torch.uint8).to(dev).contiguous()
+    B = seq.numel()
+    sizes = {"cu_windows": B + 1, "cu_tokens": B + 1, "cu_summaries": B + 1,
+             "sum_tok": totals.n_summaries}
+    sizes.update({f: totals.n_windows for f in WINDOW_FIELDS})
+    sizes.update({f: totals.n_tokens for f in TOKEN_FIELDS})
+    if bs is not None:
+        sizes["token_ids"] = totals.n_tokens
+    if out is not None:
+        arrays = out.arrays
+        if any(f not in arrays or arrays[f].numel() != max(int(n), 0) for f, n in sizes.items()):
+            raise ValueError("`out` layout has different sizes")
+    else:
+        arrays = {f: torch.empty(max(int(n), 0), dtype=_FIELD_DTYPE[f], device=dev) for f, n in sizes.items()}
+    d = LayoutDesc()
+    d.totals = totals
+    d.batch, d.window_nt, d.kmer_uniform, d.summary_token_id = B, int(window_nt), int(kmer_uniform), int(summary_token_id)
+    d.seq_nt, d.kmer, d.bases, d.err = _ptr(seq), _ptr(km), _ptr(bs), _ptr(err)
+    for f, t in arrays.items():
+        setattr(d, f, _ptr(t))
+    check("focus_layout", lib().focus_layout(C.byref(d), _stream(stream, dev)))
+    return Layout(totals, B, int(window_nt), arrays)
+
+
+def focus_compact_kv(lay: Layout, k, v, cache_k, cache_v, cache_len=None, win_ids=None,
+                     kv_tok_base: int = 0, err=None, stream=None):
+    """Append the summary K/V rows of the listed windows (all if win_ids is None)
+    to cache_k / cache_v [batch, cap, H_kv, D]; raise cache_len."""
+    d = CompactDesc()
+    d.totals = lay.totals
+    d.dtype = _dtype(k)
+    d.n_kv_heads, d.head_dim = k.shape[1], k.shape[2]
+    d.batch = lay.batch
+    d.n_win = 0 if win_ids is None else win_ids.numel()
+    d.win_ids = _ptr(win_ids)
+    for f in ("win_seq", "win_nsum", "win_cache_off", "win_sum_off", "sum_tok"):
+        setattr(d, f, _ptr(lay[f]))
+    d.k, d.v, d.kv_tok_base, d.kv_rows = _ptr(k), _ptr(v), int(kv_tok_base), k.shape[0]
+    if (cache_k.shape != cache_v.shape or cache_k.dtype != k.dtype or cache_k.shape[2:] != k.shape[1:]
+            or cache_k.shape[0] < lay.batch or v.shape != k.shape):
+        raise ValueError("cache shape/dtype does not match k, or holds fewer sequences than the layout")
+    if cache_len is not None and cache_len.numel() < lay.batch:
+        raise ValueError("cache_len needs one entry per sequence")
+    d.cache_k, d.cache_v, d.cache_cap = _ptr(cache_k), _ptr(cache_v), cache_k.shape[1]
+    d.cache_len, d.err = _ptr(cache_len), _ptr(err)
+    check("focus_compact_kv", lib().focus_compact_kv(C.byref(d), _stream(stream, k.device)))
+
+
+def _attn_desc(lay, q, k, v, cache_k, cache_v, o, lse, win_ids, qkv_tok_base, softmax_scale, mask,
+               workspace, err):
+    d = AttnDesc()
+    d.totals = lay.totals
+    d.dtype = _dtype(q)
+    d.n_heads, d.head_dim = q.shape[1], q.shape[2]
+    d.n_kv_heads = k.shape[1]
+    d.softmax_scale = float(softmax_scale)
+    d.mask = int(mask)
+    d.batch = lay.batch
+    d.n_win = 0 if win_ids is None else win_ids.numel()
+    d.win_ids = _ptr(win_ids)
+    for f in ("win_seq", "win_ntok", "win_cache_off", "win_tok_off"):
+        setattr(d, f, _ptr(lay[f]))
+    if not (q.dtype == k.dtype == v.dtype) or k.shape != v.shape or q.shape[0] != k.shape[0]:
+        raise ValueError("q/k/v shapes or dtypes disagree")
+    d.q, d.k, d.v, d.qkv_tok_base, d.qkv_rows = _ptr(q), _ptr(k), _ptr(v), int(qkv_tok_base), q.shape[0]
+    if cache_k is not None:
+        if (cache_k.dtype != q.dtype or cache_k.shape[2:] != k.shape[1:] or cache_k.shape != cache_v.shape
+                or cache_k.shape[0] < lay.batch):
+            raise ValueError("cache shape/dtype does not match k, or holds fewer sequences than the layout")
+        d.cache_k, d.cache_v, d.cache_cap = _ptr(cache_k), _ptr(cache_v), cache_k.shape[1]
+    d.o, d.lse = _ptr(o), _ptr(lse)
+    d.workspace = _ptr(workspace)
+    d.workspace_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    d.err = _ptr(err)
+    return d
+
+
+def focus_window_attn_workspace(lay: Layout, q, k, v, cache_k=None, cache_v=None, win_ids=None) -> int:
+    d = _attn_desc(lay, q, k, v, cache_k, cache_v, None, None, win_ids, 0, 0.0, FOCUS_MASK_CT, None, None)
+    return lib().focus_window_attn_workspace(C.byref(d))
+
+
+def focus_window_attn(lay: Layout, q, k, v, cache_k=None, cache_v=None, o=None, lse=None,
+                      win_ids=None, qkv_tok_base: int = 0, softmax_scale: float = 0.0,
+                      mask: int = FOCUS_MASK_CT, workspace=None, want_lse: bool = True,
+                      err=None, stream=None):
+    """Window attention over [cache ; window] for the listed windows (all if
+    win_ids is None).  q [rows, H, D], k/v [rows, H_kv, D]; returns (o, lse)."""
+    if o is None:
+        o = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty(q.shape[0], q.shape[1], dtype=torch.float32, device=q.device)
+    if o.shape != q.shape or o.dtype != q.dtype or (lse is not None and tuple(lse.shape) != tuple(q.shape[:2])):
+        raise ValueError("o must match q; lse must be [rows, heads]")
+    d = _attn_desc(lay, q, k, v, cache_k, cache_v, o, lse, win_ids, qkv_tok_base, softmax_scale,
+                   mask, workspace, err)
+    check("focus_window_attn", lib().focus_window_attn(C.byref(d), _stream(stream, q.device)))
+    return o, lse
+
+
+def _decode_desc(q, k_new, v_new, kind, cache_k, cache_v, cache_len, win_k, win_v, win_len,
+                 o, lse, workspace, split_keys, softmax_scale, err):
+    d = DecodeDesc()
+    d.dtype = _dtype(q)
+    d.batch, d.n_heads, d.head_dim = q.shape
+    d.n_kv_heads = k_new.shape[1]
+    d.softmax_scale = float(softmax_scale)
+    d.split_keys = int(split_keys)
+    d.q, d.k_new, d.v_new, d.kind = _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(kind)
+    d.cache_k, d.cache_v, d.cache_cap, d.cache_len = _ptr(cache_k), _ptr(cache_v), cache_k.shape[1], _ptr(cache_len)
+    d.win_k, d.win_v, d.win_cap, d.win_len = _ptr(win_k), _ptr(win_v), win_k.shape[1], _ptr(win_len)
+    d.o, d.lse = _ptr(o), _ptr(lse)
+    d.workspace = _ptr(workspace)
+    d.workspace_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    d.err = _ptr(err)
+    return d
+
+
+def focus_decode_workspace(q, k_new, cache_k, win_k, split_keys: int = 0) -> int:
+    d = DecodeDesc()
+    d.dtype = _dtype(q)
+    d.batch, d.n_heads, d.head_dim = q.shape
+    d.n_kv_heads = k_new.shape[1]
+    d.split_keys = int(split_keys)
+    d.cache_cap, d.win_cap = cache_k.shape[1], win_k.shape[1]
+    return lib().focus_decode_workspace(C.byref(d))
+
+
+def focus_decode_step(q, k_new, v_new, kind, cache_k, cache_v, cache_len, win_k, win_v, win_len,
+                      o=None, lse=None, workspace=None, split_keys: int = 0,
+                      softmax_scale: float = 0.0, want_lse: bool = True, err=None, stream=None):
+    """One decode step for every sequence of the batch; returns (o, lse)."""
+    if o is None:
+        o = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty(q.shape[0], q.shape[1], dtype=torch.float32, device=q.device)
+    B, H, D = q.shape
+    Hkv = k_new.shape[1]
+    if (k_new.shape != (B, Hkv, D) or v_new.shape != k_new.shape or kind.numel() < B
+            or cache_k.shape[0] < B or cache_k.shape[2:] != (Hkv, D) or cache_v.shape != cache_k.shape
+            or win_k.shape[0] < B or win_k.shape[2:] != (Hkv, D) or win_v.shape != win_k.shape
+            or cache_len.numel() < B or win_len.numel() < B or o.shape != q.shape
+            or (lse is not None and tuple(lse.shape) != (B, H))):
+        raise ValueError("decode tensor shapes disagree")
+    if workspace is None:
+        n = focus_decode_workspace(q, k_new, cache_k, win_k, split_keys)
+        workspace = torch.empty(max(n, 16), dtype=torch.uint8, device=q.device)
+    d = _decode_desc(q, k_new, v_new, kind, cache_k, cache_v, cache_len, win_k, win_v, win_len,
+                     o, lse, workspace, split_keys, softmax_scale, err)
+    check("focus_decode_step", lib().focus_decode_step(C.byref(d), _stream(stream, q.device)))
+    return o, lse

@@ -1,0 +1,450 @@
+// Window attention over [retained summary cache ; window] (focus_window_attn).
+//
+// For window w of sequence b, query row i (0 <= i < T_w) of head h attends to
+// every cache row j < C_w and to window rows u <= i: the visibility set C(t) of
+// Appendix A.1, which is also the mask of the masked-parallel form (A.1,
+// "Cross-window consistency").  One launch may cover any set of windows of any
+// sequences; each window only reads the cache rows its predecessors retained.
+//
+// bf16 path (the hot one), one workgroup = 4 waves = 128 query rows of one
+// (window, head), keys streamed in tiles of 64 through LDS, double-buffered:
+//   S^T = K Q^T   v_mfma_f32_32x32x16_bf16: each lane ends up holding one
+//                 query's scores for 16 keys of a 32-key block, so the row
+//                 max / row sum are lane-local plus one exchange with lane^32;
+//   softmax       exp2 domain, running max with lazy rescaling: the output
+//                 accumulator is rescaled only when a row's max grows by more
+//                 than 2^8, which keeps exp2 arguments <= 8 and is exact;
+//   O^T += V^T P^T  the same MFMA; P comes straight from the S^T accumulator
+//                 (rounded to bf16), V^T is read from LDS with the gfx950
+//                 transposing read ds_read_b64_tr_b16.
+// Both LDS tiles are XOR-swizzled so that the MFMA operand reads are free of
+// bank conflicts.  Blocks are dealt out so that all query tiles of one
+// (window, head) land on the same XCD (sharing K/V through its L2) and the
+// listed windows are started in list order (last window = largest cache first
+// by default).
+//
+// f32 path: a plain VALU kernel (4 lanes per query row, exact online softmax),
+// used for the float32 checks; it is not tuned.
+#include "common.h"
+
+#include <math.h>
+
+namespace {
+
+using focus::bf16x4;
+using focus::bf16x8;
+using focus::f32x16;
+
+constexpr float kLn2 = 0.69314718055994531f;
+constexpr float kLog2e = 1.44269504088896341f;
+constexpr float kMinit = -1.0e30f;  // finite start of the running max (no inf - inf)
+constexpr float kLazy = 8.0f;       // rescale when the max grows by > 2^8
+
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+struct Item {
+  int64_t list_idx;
+  int h;
+  int qt;
+  bool valid;
+};
+
+// Block -> (listed window, head, query tile).  Blocks go round robin over the
+// XCDs; the QT query tiles of pair p = list_idx * H + h all get blocks on XCD
+// p % 8, consecutive in that XCD's dispatch order, and pairs are dispatched in
+// increasing p.
+__device__ inline Item map_block(int64_t bid, int64_t n_pairs, int H, int QT) {
+  const int x = (int)(bid % focus::kXcds);
+  const int64_t s = bid / focus::kXcds;
+  Item it;
+  it.qt = (int)(s % QT);
+  const int64_t p = (s / QT) * focus::kXcds + x;
+  it.valid = p < n_pairs;
+  it.list_idx = p / H;
+  it.h = (int)(p % H);
+  return it;
+}
+
+__device__ inline int64_t listed_window(const focus_attn_desc& d, int64_t li) {
+  return d.win_ids ? (int64_t)d.win_ids[li] : d.totals.n_windows - 1 - li;
+}
+
+// ------------------------------------------------------------------ bf16 MFMA
+
+template <int D>
+struct Cfg {
+  static constexpr int kBQ = 128;                         // query rows per block
+  static constexpr int kBK = 64;                          // keys per tile
+  static constexpr int kThreads = 256;
+  static constexpr int kRB = D * 2;                       // bytes per row
+  static constexpr int kTile = kBK * kRB;                 // bytes per tile per tensor
+  static constexpr int kCh16 = kRB / 16;                  // 16-byte chunks per row
+  static constexpr int kLoads = kBK * kCh16 / kThreads;   // chunks per thread per tensor
+  static constexpr int kKsteps = D / 16;                  // MFMA k-steps of QK^T
+  static constexpr int kDtiles = D / 32;                  // 32-row blocks of O^T
+};
+
+// K tile: 16-byte chunk c of row r sits at chunk c ^ (r mod chunks-per-row).
+template <int D>
+__device__ inline int k_off(int r, int c16) {
+  return r * Cfg<D>::kRB + ((c16 ^ (r % Cfg<D>::kCh16)) << 4);
+}
+// V tile: 64-byte granule g of row r sits at granule g ^ f(r), with f chosen
+// so that the four rows one transposing read touches per half-wave fall into
+// four different 64-byte bank groups.
+template <int D>
+__device__ inline int v_off(int r, int byte) {
+  const int f = D == 128 ? (r & 3) : ((r >> 1) & 1);
+  return r * Cfg<D>::kRB + ((((byte >> 6) ^ f)) << 6) + (byte & 63);
+}
+
+template <int D>
+__global__ __launch_bounds__(256, 2) void attn_bf16(focus_attn_desc d, float sc, int64_t n_pairs, int QT) {
+  using C = Cfg<D>;
+  __shared__ __attribute__((aligned(16))) char smem[2 * 2 * C::kTile];
+
+  const int tid = threadIdx.x;
+  const Item it = map_block(blockIdx.x, n_pairs, d.n_heads, QT);
+  if (!it.valid) return;
+  const int64_t gw = listed_window(d, it.list_idx);
+  if (gw < 0 || gw >= d.totals.n_windows) {
+    if (tid == 0 && it.qt == 0) focus::raise_err(d.err, FOCUS_ERR_BOUNDS);
+    return;
+  }
+  const int T = d.win_ntok[gw];
+  const int q0 = it.qt * C::kBQ;
+  if (q0 >= T) return;
+  const int Cw = d.win_cache_off[gw];
+  const int b = d.win_seq[gw];
+  const int64_t tok0 = d.win_tok_off[gw] - d.qkv_tok_base;
+  if (b < 0 || b >= d.batch || Cw < 0 || Cw > d.cache_cap || tok0 < 0 || tok0 + T > d.qkv_rows) {
+    if (tid == 0) focus::raise_err(d.err, FOCUS_ERR_BOUNDS);
+    return;
+  }
+  const int H = d.n_heads, Hkv = d.n_kv_heads, h = it.h;
+  const int hk = h / (H / Hkv);
+  const int nwk = min(T, q0 + C::kBQ);  // window keys any query of this tile can see
+  const int nkeys = Cw + nwk;
+  const int ntiles = (nkeys + C::kBK - 1) / C::kBK;
+
+  const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, g = lane >> 5;
+  const int qi = q0 + wave * 32 + l32;  // this lane's query row inside the window
+  const int wq_lo = q0 + wave * 32, wq_hi = wq_lo + 31;
+  const bool wave_live = wq_lo < T;
+
+  // Q^T as the B operand: lane holds query l32, head_dim [16s + 8g, 16s + 8g + 8).
+  bf16x8 qf[C::kKsteps];
+  {
+    const int64_t qrow = tok0 + min(qi, T - 1);
+    const bf16x8* qp = reinterpret_cast<const bf16x8*>(
+        reinterpret_cast<const __bf16*>(d.q) + (qrow * H + h) * D);
+#pragma unroll
+    for (int s = 0; s < C::kKsteps; ++s) qf[s] = qp[2 * s + g];
+  }
+
+  const int64_t row_elems = (int64_t)Hkv * D;
+  const __bf16* kwin = reinterpret_cast<const __bf16*>(d.k) + (tok0 * Hkv + hk) * D;
+  const __bf16* vwin = reinterpret_cast<const __bf16*>(d.v) + (tok0 * Hkv + hk) * D;
+  const __bf16* kcache = reinterpret_cast<const __bf16*>(d.cache_k) + ((int64_t)b * d.cache_cap * Hkv + hk) * D;
+  const __bf16* vcache = reinterpret_cast<const __bf16*>(d.cache_v) + ((int64_t)b * d.cache_cap * Hkv + hk) * D;
+
+  uint4 rk[C::kLoads], rv[C::kLoads];
+  auto load_tile = [&](int t) {
+#pragma unroll
+    for (int i = 0; i < C::kLoads; ++i) {
+      const int c = tid + i * C::kThreads;
+      const int r = c / C::kCh16, c16 = c % C::kCh16;
+      const int j = t * C::kBK + r;
+      if (j < Cw) {
+        rk[i] = reinterpret_cast<const uint4*>(kcache + (int64_t)j * row_elems)[c16];
+        rv[i] = reinterpret_cast<const uint4*>(vcache + (int64_t)j * row_elems)[c16];
+      } else if (j < nkeys) {
+        rk[i] = reinterpret_cast<const uint4*>(kwin + (int64_t)(j - Cw) * row_elems)[c16];
+        rv[i] = reinterpret_cast<const uint4*>(vwin + (int64_t)(j - Cw) * row_elems)[c16];
+      } else {
+        rk[i] = make_uint4(0, 0, 0, 0);
+        rv[i] = make_uint4(0, 0, 0, 0);
+      }
+    }
+  };
+  auto store_tile = [&](int buf) {
+    char* kl = smem + buf * 2 * C::kTile;
+    char* vl = kl + C::kTile;
+#pragma unroll
+    for (int i = 0; i < C::kLoads; ++i) {
+      const int c = tid + i * C::kThreads;
+      const int r = c / C::kCh16, c16 = c % C::kCh16;
+      *reinterpret_cast<uint4*>(kl + k_off<D>(r, c16)) = rk[i];
+      *reinterpret_cast<uint4*>(vl + v_off<D>(r, c16 * 16)) = rv[i];
+    }
+  };
+
+  f32x16 oacc[C::kDtiles];
+#pragma unroll
+  for (int dt = 0; dt < C::kDtiles; ++dt)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) oacc[dt][v] = 0.f;
+  float m_run = kMinit, l_run = 0.f;
+
+  // transposing-read coordinates: lane = 16 * grp + 4 * ri + bq
+  const int grp = lane >> 4, ri = (lane >> 2) & 3, bq = lane & 3;
+
+  load_tile(0);
+  store_tile(0);
+  __syncthreads();
+  for (int t = 0; t < ntiles; ++t) {
+    if (t + 1 < ntiles) load_tile(t + 1);
+    const int j0 = t * C::kBK;
+    const char* kl = smem + (t & 1) * 2 * C::kTile;
+    const char* vl = kl + C::kTile;
+    if (wave_live && j0 - Cw <= wq_hi) {
+      f32x16 sacc[2];
+#pragma unroll
+      for (int st = 0; st < 2; ++st) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) sacc[st][v] = 0.f;
+        const int r = st * 32 + l32;
+#pragma unroll
+        for (int s = 0; s < C::kKsteps; ++s) {
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(kl + k_off<D>(r, 2 * s + g));
+          sacc[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[s], sacc[st], 0, 0, 0);
+        }
+      }
+      // sacc[st][v] = score of query qi with key j0 + 32 st + 8 (v/4) + 4 g + v%4
+      if (j0 + C::kBK - 1 - Cw > wq_lo) {
+#pragma unroll
+        for (int st = 0; st < 2; ++st)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int j = j0 + st * 32 + (v >> 2) * 8 + 4 * g + (v & 3);
+            if (j >= Cw && j - Cw > qi) sacc[st][v] = -INFINITY;
+          }
+      }
+      float mx = -INFINITY;
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[st][v]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float m_new = fmaxf(m_run, mx * sc);
+      if (__any(m_new - m_run > kLazy)) {
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        l_run *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < C::kDtiles; ++dt)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) oacc[dt][v] *= alpha;
+        m_run = m_new;
+      }
+      float psum = 0.f;
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(sacc[st][v], sc, -m_run));
+          sacc[st][v] = p;
+          psum += p;
+        }
+      l_run += psum;
+#pragma unroll
+      for (int st = 0; st < 2; ++st) {
+#pragma unroll
+        for (int m = 0; m < 2; ++m) {
+          bf16x8 pb;
+#pragma unroll
+          for (int v = 0; v < 8; ++v) pb[v] = (__bf16)sacc[st][8 * m + v];
+          // keys of B slot v: 32 st + 16 m + 8 (v/4) + 4 g + v%4
+          const int kb = st * 32 + 16 * m + 4 * (grp >> 1) + ri;
+#pragma unroll
+          for (int dt = 0; dt < C::kDtiles; ++dt) {
+            const int col_byte = 2 * (32 * dt + 16 * (grp & 1) + 4 * bq);
+            const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+                (lds_bf16x4*)(vl + v_off<D>(kb, col_byte)));
+            const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+                (lds_bf16x4*)(vl + v_off<D>(kb + 8, col_byte)));
+            const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+            oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, oacc[dt], 0, 0, 0);
+          }
+        }
+      }
+    }
+    if (t + 1 < ntiles) store_tile((t + 1) & 1);
+    __syncthreads();
+  }
+
+  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  if (qi < T) {
+    const float inv = 1.f / l_tot;
+    const int64_t orow = tok0 + qi;
+    __bf16* op = reinterpret_cast<__bf16*>(d.o) + (orow * H + h) * D;
+#pragma unroll
+    for (int dt = 0; dt < C::kDtiles; ++dt)
+#pragma unroll
+      for (int v4 = 0; v4 < 4; ++v4) {
+        // oacc[dt][4 v4 + e] = O[qi][32 dt + 8 v4 + 4 g + e]
+        uint2 w;
+        w.x = focus::pack_bf16x2(oacc[dt][4 * v4 + 0] * inv, oacc[dt][4 * v4 + 1] * inv);
+        w.y = focus::pack_bf16x2(oacc[dt][4 * v4 + 2] * inv, oacc[dt][4 * v4 + 3] * inv);
+        *reinterpret_cast<uint2*>(op + 32 * dt + 8 * v4 + 4 * g) = w;
+      }
+    if (g == 0 && d.lse) d.lse[orow * H + h] = (m_run + log2f(l_tot)) * kLn2;
+  }
+}
+
+// ----------------------------------------------------------------- f32 VALU
+
+template <int D>
+__global__ __launch_bounds__(256) void attn_f32(focus_attn_desc d, float sc, int64_t n_pairs, int QT) {
+  constexpr int kBQ = 64, kBK = 32, kF4 = D / 4, kPer = D / 16;  // float4 per row / per lane
+  __shared__ float4 ks[kBK][kF4];
+  __shared__ float4 vs[kBK][kF4];
+
+  const int tid = threadIdx.x;
+  const Item it = map_block(blockIdx.x, n_pairs, d.n_heads, QT);
+  if (!it.valid) return;
+  const int64_t gw = listed_window(d, it.list_idx);
+  if (gw < 0 || gw >= d.totals.n_windows) {
+    if (tid == 0 && it.qt == 0) focus::raise_err(d.err, FOCUS_ERR_BOUNDS);
+    return;
+  }
+  const int T = d.win_ntok[gw];
+  const int q0 = it.qt * kBQ;
+  if (q0 >= T) return;
+  const int Cw = d.win_cache_off[gw];
+  const int b = d.win_seq[gw];
+  const int64_t tok0 = d.win_tok_off[gw] - d.qkv_tok_base;
+  if (b < 0 || b >= d.batch || Cw < 0 || Cw > d.cache_cap || tok0 < 0 || tok0 + T > d.qkv_rows) {
+    if (tid == 0) focus::raise_err(d.err, FOCUS_ERR_BOUNDS);
+    return;
+  }
+  const int H = d.n_heads, Hkv = d.n_kv_heads, h = it.h;
+  const int hk = h / (H / Hkv);
+  const int nkeys = Cw + min(T, q0 + kBQ);
+  const int qi = q0 + (tid >> 2), sub = tid & 3;
+  const int64_t row_f4 = (int64_t)Hkv * kF4;
+
+  float4 qv[kPer], ov[kPer];
+  {
+    const float4* qp = reinterpret_cast<const float4*>(d.q) + (tok0 + min(qi, T - 1)) * H * kF4 + h * kF4;
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      qv[i] = qp[4 * i + sub];
+      ov[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  }
+  const float4* kwin = reinterpret_cast<const float4*>(d.k) + tok0 * row_f4 + hk * kF4;
+  const float4* vwin = reinterpret_cast<const float4*>(d.v) + tok0 * row_f4 + hk * kF4;
+  const float4* kcache = reinterpret_cast<const float4*>(d.cache_k) + (int64_t)b * d.cache_cap * row_f4 + hk * kF4;
+  const float4* vcache = reinterpret_cast<const float4*>(d.cache_v) + (int64_t)b * d.cache_cap * row_f4 + hk * kF4;
+
+  float m = kMinit, l = 0.f;
+  for (int j0 = 0; j0 < nkeys; j0 += kBK) {
+    __syncthreads();
+    for (int c = tid; c < kBK * kF4; c += 256) {
+      const int r = c / kF4, c4 = c % kF4, j = j0 + r;
+      float4 kx = make_float4(0.f, 0.f, 0.f, 0.f), vx = kx;
+      if (j < Cw) {
+        kx = kcache[(int64_t)j * row_f4 + c4];
+        vx = vcache[(int64_t)j * row_f4 + c4];
+      } else if (j < nkeys) {
+        kx = kwin[(int64_t)(j - Cw) * row_f4 + c4];
+        vx = vwin[(int64_t)(j - Cw) * row_f4 + c4];
+      }
+      ks[r][c4] = kx;
+      vs[r][c4] = vx;
+    }
+    __syncthreads();
+    const int kend = min(kBK, nkeys - j0);
+    for (int kk = 0; kk < kend; ++kk) {
+      float s = 0.f;
+#pragma unroll
+      for (int i = 0; i < kPer; ++i) {
+        const float4 kx = ks[kk][4 * i + sub];
+        s = fmaf(qv[i].x, kx.x, s);
+        s = fmaf(qv[i].y, kx.y, s);
+        s = fmaf(qv[i].z, kx.z, s);
+        s = fmaf(qv[i].w, kx.w, s);
+      }
+      s = focus::sum4(s) * sc;
+      const int j = j0 + kk;
+      if (j < Cw || j - Cw <= qi) {
+        const float m_new = fmaxf(m, s);
+        const float corr = __builtin_amdgcn_exp2f(m - m_new);
+        const float p = __builtin_amdgcn_exp2f(s - m_new);
+        l = l * corr + p;
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+          const float4 vx = vs[kk][4 * i + sub];
+          ov[i].x = fmaf(p, vx.x, ov[i].x * corr);
+          ov[i].y = fmaf(p, vx.y, ov[i].y * corr);
+          ov[i].z = fmaf(p, vx.z, ov[i].z * corr);
+          ov[i].w = fmaf(p, vx.w, ov[i].w * corr);
+        }
+        m = m_new;
+      }
+    }
+  }
+  if (qi < T) {
+    const float inv = 1.f / l;
+    float4* op = reinterpret_cast<float4*>(d.o) + (tok0 + qi) * H * kF4 + h * kF4;
+#pragma unroll
+    for (int i = 0; i < kPer; ++i)
+      op[4 * i + sub] = make_float4(ov[i].x * inv, ov[i].y * inv, ov[i].z * inv, ov[i].w * inv);
+    if (sub == 0 && d.lse) d.lse[(tok0 + qi) * H + h] = (m + log2f(l)) * kLn2;
+  }
+}
+
+}  // namespace
+
+extern "C" size_t focus_window_attn_workspace(const focus_attn_desc* d) {
+  (void)d;
+  return 0;
+}
+
+extern "C" focus_status focus_window_attn(const focus_attn_desc* d, focus_stream_t stream) {
+  if (!d) return FOCUS_E_NULL;
+  if (d->dtype != FOCUS_BF16 && d->dtype != FOCUS_F32) return FOCUS_E_DTYPE;
+  if (d->mask == FOCUS_MASK_KMER_LOCAL) return FOCUS_E_UNSUPPORTED;
+  if (d->mask != FOCUS_MASK_CT) return FOCUS_E_ARG;
+  if (d->n_heads <= 0 || d->n_kv_heads <= 0 || d->batch < 0 || d->cache_cap < 0 ||
+      d->qkv_rows < 0 || (d->win_ids && d->n_win < 0) || !(d->softmax_scale == d->softmax_scale))
+    return FOCUS_E_ARG;
+  if (d->head_dim != 64 && d->head_dim != 128) return FOCUS_E_UNSUPPORTED;
+  if (d->n_heads % d->n_kv_heads) return FOCUS_E_SHAPE;
+  const focus_layout_totals& t = d->totals;
+  if (t.n_windows < 0 || t.max_window_tokens < 0 || t.max_window_cache < 0) return FOCUS_E_SHAPE;
+  const int64_t nwl = d->win_ids ? d->n_win : t.n_windows;
+  if (nwl == 0 || t.max_window_tokens == 0) return FOCUS_OK;
+  if (!d->win_seq || !d->win_ntok || !d->win_cache_off || !d->win_tok_off || !d->q || !d->k ||
+      !d->v || !d->o)
+    return FOCUS_E_NULL;
+  if (t.max_window_cache > 0 && (!d->cache_k || !d->cache_v)) return FOCUS_E_NULL;
+  if (!focus::aligned16(d->q) || !focus::aligned16(d->k) || !focus::aligned16(d->v) ||
+      !focus::aligned16(d->o) || !focus::aligned16(d->cache_k) || !focus::aligned16(d->cache_v) ||
+      (reinterpret_cast<uintptr_t>(d->lse) & 3u))
+    return FOCUS_E_ARG;
+  if (!d->win_ids && t.max_window_cache > d->cache_cap) return FOCUS_E_CAPACITY;
+  if (focus_window_attn_workspace(d) > d->workspace_bytes) return FOCUS_E_WORKSPACE;
+
+  const float scale = d->softmax_scale > 0.f ? d->softmax_scale : 1.0f / sqrtf((float)d->head_dim);
+  const float sc = scale * kLog2e;
+  const int64_t n_pairs = nwl * d->n_heads;
+  const int bq = d->dtype == FOCUS_BF16 ? 128 : 64;
+  const int64_t qt = focus::ceil_div(t.max_window_tokens, bq);
+  const int64_t blocks = focus::ceil_div(n_pairs, focus::kXcds) * focus::kXcds * qt;
+  if (blocks * 256 >= ((int64_t)1 << 32) || qt > INT32_MAX) return FOCUS_E_SHAPE;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const dim3 grid((uint32_t)blocks), block(256);
+  if (d->dtype == FOCUS_BF16) {
+    if (d->head_dim == 128)
+      hipLaunchKernelGGL(attn_bf16<128>, grid, block, 0, s, *d, sc, n_pairs, (int)qt);
+    else
+      hipLaunchKernelGGL(attn_bf16<64>, grid, block, 0, s, *d, sc, n_pairs, (int)qt);
+  } else {
+    if (d->head_dim == 128)
+      hipLaunchKernelGGL(attn_f32<128>, grid, block, 0, s, *d, sc, n_pairs, (int)qt);
+    else
+      hipLaunchKernelGGL(attn_f32<64>, grid, block, 0, s, *d, sc, n_pairs, (int)qt);
+  }
+  return focus::launch_status();
+}
