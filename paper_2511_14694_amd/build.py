@@ -64,7 +64,7 @@ def build(verbose: bool = False, save_temps: bool = False) -> str:
             objs.append(obj)
             cmd = [hipcc, *HIPCC_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
             if save_temps:
-                cmd.insert(1, f"-save-temps={BUILD}")
+                cmd.insert(1, "-save-temps=obj")
             jobs.append(ex.submit(_run, cmd, verbose))
         for j in jobs:
             j.result()

@@ -34,6 +34,7 @@ namespace {
 using focus::bf16x4;
 using focus::bf16x8;
 using focus::f32x16;
+using focus::u32x4;
 
 constexpr float kLn2 = 0.69314718055994531f;
 constexpr float kLog2e = 1.44269504088896341f;
@@ -41,6 +42,10 @@ constexpr float kMinit = -1.0e30f;  // finite start of the running max (no inf -
 constexpr float kLazy = 8.0f;       // rescale when the max grows by > 2^8
 
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Waves per workgroup of the bf16 kernel (each wave owns 32 query rows).
+constexpr int kBf16Waves = 8;
 
 struct Item {
   int64_t list_idx;
@@ -71,11 +76,12 @@ __device__ inline int64_t listed_window(const focus_attn_desc& d, int64_t li) {
 
 // ------------------------------------------------------------------ bf16 MFMA
 
-template <int D>
+template <int D, int W>
 struct Cfg {
-  static constexpr int kBQ = 128;                         // query rows per block
+  static constexpr int kWaves = W;                        // 32 query rows per wave
+  static constexpr int kBQ = 32 * W;                      // query rows per block
   static constexpr int kBK = 64;                          // keys per tile
-  static constexpr int kThreads = 256;
+  static constexpr int kThreads = 64 * W;
   static constexpr int kRB = D * 2;                       // bytes per row
   static constexpr int kTile = kBK * kRB;                 // bytes per tile per tensor
   static constexpr int kCh16 = kRB / 16;                  // 16-byte chunks per row
@@ -87,7 +93,8 @@ struct Cfg {
 // K tile: 16-byte chunk c of row r sits at chunk c ^ (r mod chunks-per-row).
 template <int D>
 __device__ inline int k_off(int r, int c16) {
-  return r * Cfg<D>::kRB + ((c16 ^ (r % Cfg<D>::kCh16)) << 4);
+  constexpr int kRB = D * 2, kCh16 = kRB / 16;
+  return r * kRB + ((c16 ^ (r % kCh16)) << 4);
 }
 // V tile: 64-byte granule g of row r sits at granule g ^ f(r), with f chosen
 // so that the four rows one transposing read touches per half-wave fall into
@@ -95,13 +102,17 @@ __device__ inline int k_off(int r, int c16) {
 template <int D>
 __device__ inline int v_off(int r, int byte) {
   const int f = D == 128 ? (r & 3) : ((r >> 1) & 1);
-  return r * Cfg<D>::kRB + ((((byte >> 6) ^ f)) << 6) + (byte & 63);
+  return r * (D * 2) + ((((byte >> 6) ^ f)) << 6) + (byte & 63);
 }
 
-template <int D>
-__global__ __launch_bounds__(256, 2) void attn_bf16(focus_attn_desc d, float sc, int64_t n_pairs, int QT) {
-  using C = Cfg<D>;
-  __shared__ __attribute__((aligned(16))) char smem[2 * 2 * C::kTile];
+template <int D, int W>
+__global__ __launch_bounds__(64 * W, 2) void attn_bf16(focus_attn_desc d, float sc, int64_t n_pairs, int QT) {
+  using C = Cfg<D, W>;
+  // Two K and two V tile buffers as separate arrays, referenced statically by
+  // a loop unrolled by two: the compiler can then tell a tile being read from
+  // the one being filled, and waits for the copies only at the barrier.
+  __shared__ __attribute__((aligned(1024))) char kbuf0[C::kTile], kbuf1[C::kTile];
+  __shared__ __attribute__((aligned(1024))) char vbuf0[C::kTile], vbuf1[C::kTile];
 
   const int tid = threadIdx.x;
   const Item it = map_block(blockIdx.x, n_pairs, d.n_heads, QT);
@@ -124,8 +135,11 @@ __global__ __launch_bounds__(256, 2) void attn_bf16(focus_attn_desc d, float sc,
   const int H = d.n_heads, Hkv = d.n_kv_heads, h = it.h;
   const int hk = h / (H / Hkv);
   const int nwk = min(T, q0 + C::kBQ);  // window keys any query of this tile can see
-  const int nkeys = Cw + nwk;
-  const int ntiles = (nkeys + C::kBK - 1) / C::kBK;
+  // Keys are visited as nct tiles of cache rows [0, Cw) followed by nwt tiles
+  // of window rows [0, nwk); only the last tile of each phase is partial.
+  const int nct = (Cw + C::kBK - 1) / C::kBK;
+  const int nwt = (nwk + C::kBK - 1) / C::kBK;
+  const int ntiles = nct + nwt;
 
   const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, g = lane >> 5;
   const int qi = q0 + wave * 32 + l32;  // this lane's query row inside the window
@@ -142,40 +156,51 @@ __global__ __launch_bounds__(256, 2) void attn_bf16(focus_attn_desc d, float sc,
     for (int s = 0; s < C::kKsteps; ++s) qf[s] = qp[2 * s + g];
   }
 
-  const int64_t row_elems = (int64_t)Hkv * D;
-  const __bf16* kwin = reinterpret_cast<const __bf16*>(d.k) + (tok0 * Hkv + hk) * D;
-  const __bf16* vwin = reinterpret_cast<const __bf16*>(d.v) + (tok0 * Hkv + hk) * D;
-  const __bf16* kcache = reinterpret_cast<const __bf16*>(d.cache_k) + ((int64_t)b * d.cache_cap * Hkv + hk) * D;
-  const __bf16* vcache = reinterpret_cast<const __bf16*>(d.cache_v) + ((int64_t)b * d.cache_cap * Hkv + hk) * D;
+  // Tiles move global -> LDS directly (global_load_lds_dwordx4: one wave
+  // instruction fills 1 KB of LDS, lane l its 16 bytes at offset 16 l), so no
+  // registers or LDS writes are spent on staging.  Wave-load i of wave w fills
+  // tile rows (w kDma + i) kRPK + lane / kCh16; the lane at 16-byte slot p of
+  // a row fetches the global chunk the swizzled layout keeps there.  Tile base
+  // pointers are uniform; per-lane parts are 32-bit byte offsets.  The last
+  // tile of a phase clamps its rows to the last valid one (extra rows are
+  // masked; the clamp keeps reads inside the buffers).
+  constexpr int kRPK = 1024 / C::kRB;
+  constexpr int kDma = C::kTile / 1024 / C::kWaves;
+  static_assert(kDma >= 1 && C::kTile % (1024 * C::kWaves) == 0, "tile must split into 1 KB wave loads");
+  const uint32_t row_bytes = (uint32_t)(Hkv * D * 2);
+  uint32_t rowb[kDma], kchunk[kDma], vchunk[kDma];
+#pragma unroll
+  for (int i = 0; i < kDma; ++i) {
+    const int r = (wave * kDma + i) * kRPK + lane / C::kCh16;
+    const int p = lane % C::kCh16;
+    const int f = D == 128 ? (r & 3) : ((r >> 1) & 1);
+    rowb[i] = (uint32_t)r * row_bytes;
+    kchunk[i] = (uint32_t)((p ^ (r % C::kCh16)) * 16);
+    vchunk[i] = (uint32_t)((((p >> 2) ^ f) * 4 + (p & 3)) * 16);
+  }
+  const char* kwin = reinterpret_cast<const char*>(reinterpret_cast<const __bf16*>(d.k) + (tok0 * Hkv + hk) * D);
+  const char* vwin = reinterpret_cast<const char*>(reinterpret_cast<const __bf16*>(d.v) + (tok0 * Hkv + hk) * D);
+  const char* kcache = reinterpret_cast<const char*>(
+      reinterpret_cast<const __bf16*>(d.cache_k) + ((int64_t)b * d.cache_cap * Hkv + hk) * D);
+  const char* vcache = reinterpret_cast<const char*>(
+      reinterpret_cast<const __bf16*>(d.cache_v) + ((int64_t)b * d.cache_cap * Hkv + hk) * D);
 
-  uint4 rk[C::kLoads], rv[C::kLoads];
-  auto load_tile = [&](int t) {
+  // Tile x lives in buffers x & 1.
+  auto issue_tile = [&](int t, char* kbuf, char* vbuf) {
+    const bool in_cache = t < nct;
+    const int row0 = in_cache ? t * C::kBK : (t - nct) * C::kBK;
+    const int nvalid = (in_cache ? Cw : nwk) - row0;
+    const char* kb = (in_cache ? kcache : kwin) + (int64_t)row0 * row_bytes;
+    const char* vb = (in_cache ? vcache : vwin) + (int64_t)row0 * row_bytes;
+    char* kl = kbuf + wave * kDma * 1024;
+    char* vl = vbuf + wave * kDma * 1024;
+    const uint32_t last = (uint32_t)(nvalid - 1) * row_bytes;
 #pragma unroll
-    for (int i = 0; i < C::kLoads; ++i) {
-      const int c = tid + i * C::kThreads;
-      const int r = c / C::kCh16, c16 = c % C::kCh16;
-      const int j = t * C::kBK + r;
-      if (j < Cw) {
-        rk[i] = reinterpret_cast<const uint4*>(kcache + (int64_t)j * row_elems)[c16];
-        rv[i] = reinterpret_cast<const uint4*>(vcache + (int64_t)j * row_elems)[c16];
-      } else if (j < nkeys) {
-        rk[i] = reinterpret_cast<const uint4*>(kwin + (int64_t)(j - Cw) * row_elems)[c16];
-        rv[i] = reinterpret_cast<const uint4*>(vwin + (int64_t)(j - Cw) * row_elems)[c16];
-      } else {
-        rk[i] = make_uint4(0, 0, 0, 0);
-        rv[i] = make_uint4(0, 0, 0, 0);
-      }
-    }
-  };
-  auto store_tile = [&](int buf) {
-    char* kl = smem + buf * 2 * C::kTile;
-    char* vl = kl + C::kTile;
-#pragma unroll
-    for (int i = 0; i < C::kLoads; ++i) {
-      const int c = tid + i * C::kThreads;
-      const int r = c / C::kCh16, c16 = c % C::kCh16;
-      *reinterpret_cast<uint4*>(kl + k_off<D>(r, c16)) = rk[i];
-      *reinterpret_cast<uint4*>(vl + v_off<D>(r, c16 * 16)) = rv[i];
+    for (int i = 0; i < kDma; ++i) {
+      const uint32_t rb = nvalid >= C::kBK ? rowb[i] : min(rowb[i], last);
+      const uint32_t ko = rb + kchunk[i], vo = rb + vchunk[i];
+      __builtin_amdgcn_global_load_lds(kb + ko, (lds_void*)(kl + i * 1024), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(vb + vo, (lds_void*)(vl + i * 1024), 16, 0, 0);
     }
   };
 
@@ -189,15 +214,15 @@ __global__ __launch_bounds__(256, 2) void attn_bf16(focus_attn_desc d, float sc,
   // transposing-read coordinates: lane = 16 * grp + 4 * ri + bq
   const int grp = lane >> 4, ri = (lane >> 2) & 3, bq = lane & 3;
 
-  load_tile(0);
-  store_tile(0);
-  __syncthreads();
-  for (int t = 0; t < ntiles; ++t) {
-    if (t + 1 < ntiles) load_tile(t + 1);
-    const int j0 = t * C::kBK;
-    const char* kl = smem + (t & 1) * 2 * C::kTile;
-    const char* vl = kl + C::kTile;
-    if (wave_live && j0 - Cw <= wq_hi) {
+  auto compute_tile = [&](int t, const char* kl, const char* vl) {
+    // Key kk of the tile (0..63) is visible to this lane's query iff kk <= lim:
+    // cache tiles hide only rows past Cw, window tiles are causal.
+    const bool in_cache = t < nct;
+    const int row0 = in_cache ? t * C::kBK : (t - nct) * C::kBK;
+    const bool live = wave_live && (in_cache || row0 <= wq_hi);
+    const bool need_mask = in_cache ? row0 + C::kBK > Cw : row0 + C::kBK - 1 > wq_lo;
+    const int lim = in_cache ? Cw - row0 - 1 : qi - row0;
+    if (live) {
       f32x16 sacc[2];
 #pragma unroll
       for (int st = 0; st < 2; ++st) {
@@ -210,15 +235,14 @@ __global__ __launch_bounds__(256, 2) void attn_bf16(focus_attn_desc d, float sc,
           sacc[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[s], sacc[st], 0, 0, 0);
         }
       }
-      // sacc[st][v] = score of query qi with key j0 + 32 st + 8 (v/4) + 4 g + v%4
-      if (j0 + C::kBK - 1 - Cw > wq_lo) {
+      // sacc[st][v] = score of query qi with tile key 32 st + 8 (v/4) + 4 g + v%4
+      if (need_mask) {
+        const int lim_g = lim - 4 * g;
 #pragma unroll
         for (int st = 0; st < 2; ++st)
 #pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const int j = j0 + st * 32 + (v >> 2) * 8 + 4 * g + (v & 3);
-            if (j >= Cw && j - Cw > qi) sacc[st][v] = -INFINITY;
-          }
+          for (int v = 0; v < 16; ++v)
+            if (st * 32 + (v >> 2) * 8 + (v & 3) > lim_g) sacc[st][v] = -INFINITY;
       }
       float mx = -INFINITY;
 #pragma unroll
@@ -268,7 +292,18 @@ __global__ __launch_bounds__(256, 2) void attn_bf16(focus_attn_desc d, float sc,
         }
       }
     }
-    if (t + 1 < ntiles) store_tile((t + 1) & 1);
+  };
+
+  // The barrier closing each step also waits for the next tile's copies.
+  issue_tile(0, kbuf0, vbuf0);
+  __syncthreads();
+  for (int t = 0; t < ntiles; t += 2) {
+    if (t + 1 < ntiles) issue_tile(t + 1, kbuf1, vbuf1);
+    compute_tile(t, kbuf0, vbuf0);
+    __syncthreads();
+    if (t + 1 >= ntiles) break;
+    if (t + 2 < ntiles) issue_tile(t + 2, kbuf0, vbuf0);
+    compute_tile(t + 1, kbuf1, vbuf1);
     __syncthreads();
   }
 
@@ -429,17 +464,18 @@ extern "C" focus_status focus_window_attn(const focus_attn_desc* d, focus_stream
   const float scale = d->softmax_scale > 0.f ? d->softmax_scale : 1.0f / sqrtf((float)d->head_dim);
   const float sc = scale * kLog2e;
   const int64_t n_pairs = nwl * d->n_heads;
-  const int bq = d->dtype == FOCUS_BF16 ? 128 : 64;
+  const int bq = d->dtype == FOCUS_BF16 ? 32 * kBf16Waves : 64;
+  const int threads = d->dtype == FOCUS_BF16 ? 64 * kBf16Waves : 256;
   const int64_t qt = focus::ceil_div(t.max_window_tokens, bq);
   const int64_t blocks = focus::ceil_div(n_pairs, focus::kXcds) * focus::kXcds * qt;
-  if (blocks * 256 >= ((int64_t)1 << 32) || qt > INT32_MAX) return FOCUS_E_SHAPE;
+  if (blocks * threads >= ((int64_t)1 << 32) || qt > INT32_MAX) return FOCUS_E_SHAPE;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  const dim3 grid((uint32_t)blocks), block(256);
+  const dim3 grid((uint32_t)blocks), block(threads);
   if (d->dtype == FOCUS_BF16) {
     if (d->head_dim == 128)
-      hipLaunchKernelGGL(attn_bf16<128>, grid, block, 0, s, *d, sc, n_pairs, (int)qt);
+      hipLaunchKernelGGL((attn_bf16<128, kBf16Waves>), grid, block, 0, s, *d, sc, n_pairs, (int)qt);
     else
-      hipLaunchKernelGGL(attn_bf16<64>, grid, block, 0, s, *d, sc, n_pairs, (int)qt);
+      hipLaunchKernelGGL((attn_bf16<64, kBf16Waves>), grid, block, 0, s, *d, sc, n_pairs, (int)qt);
   } else {
     if (d->head_dim == 128)
       hipLaunchKernelGGL(attn_f32<128>, grid, block, 0, s, *d, sc, n_pairs, (int)qt);
