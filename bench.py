@@ -140,6 +140,8 @@ def cpu_baseline(torch, s, budget_s=20.0):
     t_layout = time.perf_counter() - t_layout0
     nw = ref["n_windows"]
     order = [nw - 1, nw // 2, nw // 4, 3 * nw // 4, 1]
+    stride = next(p for p in (379, 383, 389, 397) if nw % p)   # co-prime: visits every window
+    order += [i for i in ((j * stride) % nw for j in range(nw)) if i not in order]
     done, pairs, t_attn = [], 0, 0.0
     for wi in order:
         t0, T = int(ref["win_tok_off"][wi]), int(ref["win_ntok"][wi])
@@ -158,10 +160,14 @@ def cpu_baseline(torch, s, budget_s=20.0):
     total_pairs = visible_pairs(ref["win_ntok"], ref["win_cache_off"])
     t_full = t_attn * total_pairs / pairs + t_layout
     return {"value": w.seq_nt * w.batch / t_full, "unit": "nt/s", "cores": int(cores), "kind": "oracle",
-            "sample": (f"oracle window attention on windows {done} (all {w.heads} heads, "
+            "sample": (f"oracle window attention on {len(done)} windows {_span(done)} (all {w.heads} heads, "
                        f"{pairs:,} of {total_pairs:,} visible pairs per head) in {t_attn:.1f} s, "
                        f"plus the full oracle layout walk ({t_layout:.1f} s); full-workload time "
                        f"extrapolated by the visible-pair ratio to {t_full:.0f} s")}
+
+
+def _span(ids, show=6):
+    return str(ids) if len(ids) <= show else "[" + ", ".join(map(str, ids[:show])) + ", ...]"
 
 
 def fw_kmer(w):

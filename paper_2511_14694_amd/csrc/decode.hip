@@ -8,9 +8,11 @@
 //                   rows) reads those rows for every head -- contiguous 8 KB
 //                   K and V rows at 32 x 128 bf16 -- and writes an unnormalised
 //                   partial (running max, sum, output) per head
-//   decode_combine  one workgroup per sequence merges the partials with
-//                   log-sum-exp weights, writes o and lse, then empties the
-//                   window buffer when the token closed its window
+//   decode_combine  one workgroup per (sequence, head) merges the partials
+//                   with log-sum-exp weights and writes o and lse; the first
+//                   head's workgroup empties the window buffer when the token
+//                   closed its window (the key count comes from the workspace,
+//                   so no workgroup reads the length it resets)
 // The step reads every cached byte exactly once, so it is HBM bound: a thread
 // owns 16 elements of one head (32 B per row in bf16) and the 8 (head_dim 128)
 // or 4 (64) threads of a head reduce their dot products with DPP.
@@ -28,10 +30,12 @@ constexpr int kThreads = 256;
 
 template <typename T> struct Elt;
 // kU4: 16-byte loads per kEpt elements; kChunk: keys loaded per online-softmax
-// update (bounded by registers: kChunk * kU4 * 2 uint4 per thread).
+// update (bounded by registers: kChunk * kU4 * 2 uint4 per thread; for bf16 the
+// 16-key chunk fills the 256 VGPRs of a one-wave-per-SIMD launch, which keeps
+// the most loads in flight).
 template <> struct Elt<__bf16> {
   static constexpr int kU4 = kEpt * 2 / 16;
-  static constexpr int kChunk = 8;
+  static constexpr int kChunk = 16;
   __device__ static void unpack(const uint4* src, float* out) {
 #pragma unroll
     for (int i = 0; i < kU4; ++i) {
@@ -108,7 +112,8 @@ __global__ __launch_bounds__(256) void decode_append(focus_decode_desc d, int64_
 // Partial attention of one (sequence, split, group of kThreads / TPH heads).
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads) void decode_partial(focus_decode_desc d, float sc, int split,
-                                                           int n_split, float* ws_o, float* ws_ml) {
+                                                           int n_split, float* ws_o, float* ws_ml,
+                                                           int32_t* ws_n) {
   constexpr int TPH = D / kEpt;
   constexpr int HPB = kThreads / TPH;
   const int n_hg = (d.n_heads + HPB - 1) / HPB;
@@ -120,6 +125,9 @@ __global__ __launch_bounds__(kThreads) void decode_partial(focus_decode_desc d, 
   const int clen = clamp_len(d.cache_len, b, d.cache_cap);
   const int wlen = clamp_len(d.win_len, b, d.win_cap);
   const int n = clen + wlen;
+  // the key count goes to the workspace, so the combine never reads win_len
+  // (which it resets at a window end)
+  if (c == 0 && hg == 0 && threadIdx.x == 0) ws_n[b] = n;
   const int jb = c * split;
   if (jb >= n) return;
   const int je = min(n, jb + split);
@@ -195,59 +203,36 @@ __global__ __launch_bounds__(kThreads) void decode_partial(focus_decode_desc d, 
   }
 }
 
+// Log-sum-exp merge of the partials of one (sequence, head): block
+// (b * H + h), one thread per output element.  The key count comes from the
+// workspace; block (b, 0) then empties the window buffer at a window end.
 template <typename T, int D>
-__device__ void combine_head(const focus_decode_desc& d, int b, int h, int sub, int ns, int n_split,
-                             const float* ws_o, const float* ws_ml) {
+__global__ __launch_bounds__(D) void decode_combine(focus_decode_desc d, int split, int n_split,
+                                                    const float* ws_o, const float* ws_ml,
+                                                    const int32_t* ws_n) {
   const int H = d.n_heads;
+  const int b = blockIdx.x / H, h = blockIdx.x % H, e = threadIdx.x;
+  const int ns = (ws_n[b] + split - 1) / split;
+  const int64_t slot0 = (int64_t)b * n_split * H + h;
   float M = kMinit;
-  for (int c = 0; c < ns; ++c) M = fmaxf(M, ws_ml[2 * (((int64_t)b * n_split + c) * H + h)]);
-  float L = 0.f, o[kEpt];
-#pragma unroll
-  for (int e = 0; e < kEpt; ++e) o[e] = 0.f;
+  for (int c = 0; c < ns; ++c) M = fmaxf(M, ws_ml[2 * (slot0 + (int64_t)c * H)]);
+  float L = 0.f, o = 0.f;
   for (int c = 0; c < ns; ++c) {
-    const int64_t slot = ((int64_t)b * n_split + c) * H + h;
+    const int64_t slot = slot0 + (int64_t)c * H;
     const float w = __builtin_amdgcn_exp2f(ws_ml[2 * slot] - M);
     L = fmaf(ws_ml[2 * slot + 1], w, L);
-    const float4* po = reinterpret_cast<const float4*>(ws_o + slot * D + sub * kEpt);
-#pragma unroll
-    for (int i = 0; i < kEpt / 4; ++i) {
-      const float4 x = po[i];
-      o[4 * i] = fmaf(x.x, w, o[4 * i]);
-      o[4 * i + 1] = fmaf(x.y, w, o[4 * i + 1]);
-      o[4 * i + 2] = fmaf(x.z, w, o[4 * i + 2]);
-      o[4 * i + 3] = fmaf(x.w, w, o[4 * i + 3]);
-    }
+    o = fmaf(ws_o[slot * D + e], w, o);
   }
-  const float inv = L > 0.f ? 1.f / L : 0.f;
-#pragma unroll
-  for (int e = 0; e < kEpt; ++e) o[e] *= inv;
-  Elt<T>::store(o, reinterpret_cast<T*>(d.o) + ((int64_t)b * H + h) * D + sub * kEpt);
-  if (sub == 0 && d.lse) d.lse[(int64_t)b * H + h] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
-}
-
-// Log-sum-exp merge of the partials of sequence blockIdx.x, all heads (one
-// block per sequence, so the window reset below cannot race a reader).
-template <typename T, int D>
-__global__ __launch_bounds__(kThreads) void decode_combine(focus_decode_desc d, int split, int n_split,
-                                                           const float* ws_o, const float* ws_ml) {
-  constexpr int TPH = D / kEpt;
-  constexpr int HPB = kThreads / TPH;
-  const int b = blockIdx.x;
-  const int H = d.n_heads;
-  const int n = clamp_len(d.cache_len, b, d.cache_cap) + clamp_len(d.win_len, b, d.win_cap);
-  const int ns = (n + split - 1) / split;
-  for (int h0 = 0; h0 < H; h0 += HPB) {
-    const int h = h0 + threadIdx.x / TPH, sub = threadIdx.x % TPH;
-    if (h < H) combine_head<T, D>(d, b, h, sub, ns, n_split, ws_o, ws_ml);
-  }
-  __syncthreads();
-  if (threadIdx.x == 0 && (d.kind[b] & FOCUS_STEP_WINDOW_END)) d.win_len[b] = 0;
+  o = L > 0.f ? o / L : 0.f;
+  reinterpret_cast<T*>(d.o)[((int64_t)b * H + h) * D + e] = (T)o;
+  if (e == 0 && d.lse) d.lse[(int64_t)b * H + h] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
+  if (e == 0 && h == 0 && (d.kind[b] & FOCUS_STEP_WINDOW_END)) d.win_len[b] = 0;
 }
 
 int auto_split(int64_t batch, int64_t cap) {
-  // About 1 000 workgroups for a full cache: enough to fill 256 CUs several
-  // times over while keeping the partials small.
-  int64_t s = focus::ceil_div(batch * cap, 1024);
+  // About 700 workgroups for a full cache: a few per CU, each streaming a few
+  // hundred keys so the per-split prologue and partial write stay small.
+  int64_t s = focus::ceil_div(batch * cap, 704);
   s = focus::ceil_div(s, 16) * 16;
   return (int)(s < 16 ? 16 : s > 1024 ? 1024 : s);
 }
@@ -257,6 +242,7 @@ struct Plan {
   int n_split;
   size_t ws_bytes;
   size_t ml_offset;
+  size_t n_offset;
 };
 
 Plan make_plan(const focus_decode_desc* d) {
@@ -266,7 +252,8 @@ Plan make_plan(const focus_decode_desc* d) {
   p.n_split = (int)focus::ceil_div(cap > 0 ? cap : 1, p.split);
   const size_t slots = (size_t)d->batch * p.n_split * d->n_heads;
   p.ml_offset = slots * d->head_dim * sizeof(float);
-  p.ws_bytes = p.ml_offset + slots * 2 * sizeof(float);
+  p.n_offset = p.ml_offset + slots * 2 * sizeof(float);
+  p.ws_bytes = p.n_offset + (((size_t)d->batch * sizeof(int32_t) + 15) / 16) * 16;
   return p;
 }
 
@@ -317,13 +304,14 @@ extern "C" focus_status focus_decode_step(const focus_decode_desc* d, focus_stre
   const float sc = scale * kLog2e;
   float* ws_o = reinterpret_cast<float*>(d->workspace);
   float* ws_ml = reinterpret_cast<float*>(reinterpret_cast<char*>(d->workspace) + p.ml_offset);
+  int32_t* ws_n = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(d->workspace) + p.n_offset);
   const dim3 block(kThreads);
 #define FOCUS_DECODE_LAUNCH(T, D)                                                                  \
   hipLaunchKernelGGL((decode_partial<T, D>), dim3((uint32_t)blocks), block, 0, s, *d, sc, p.split, \
-                     p.n_split, ws_o, ws_ml);                                                      \
+                     p.n_split, ws_o, ws_ml, ws_n);                                                \
   if ((st = focus::launch_status()) != FOCUS_OK) return st;                                       \
-  hipLaunchKernelGGL((decode_combine<T, D>), dim3(d->batch), block, 0, s, *d, p.split, p.n_split,  \
-                     ws_o, ws_ml);
+  hipLaunchKernelGGL((decode_combine<T, D>), dim3(d->batch * d->n_heads), dim3(D), 0, s, *d,       \
+                     p.split, p.n_split, ws_o, ws_ml, ws_n);
   if (d->dtype == FOCUS_BF16) {
     if (d->head_dim == 128) { FOCUS_DECODE_LAUNCH(__bf16, 128) } else { FOCUS_DECODE_LAUNCH(__bf16, 64) }
   } else {

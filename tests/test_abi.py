@@ -163,7 +163,8 @@ def test_decode_workspace_size_formula():
     d = _decode_ok()
     d.split_keys = 32
     n_split = -(-(100 + 10) // 32)
-    assert _abi.lib().focus_decode_workspace(C.byref(d)) == 2 * n_split * 4 * (128 + 2) * 4
+    # partials (o, max, sum) per (sequence, split, head) + one key count per sequence
+    assert _abi.lib().focus_decode_workspace(C.byref(d)) == 2 * n_split * 4 * (128 + 2) * 4 + 16
     d.head_dim = 80
     assert _abi.lib().focus_decode_workspace(C.byref(d)) == 0
 
