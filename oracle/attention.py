@@ -23,6 +23,20 @@ What is computed, in float64:
 * dense_causal: textbook causal attention, to which FOCUS attention reduces
   with no summary tokens and a single window.
 
+* The k-mer-local rule of Section 3.2 ("Visibility and summarization rule"),
+  the paper's other visibility statement: a base token sees the earlier tokens
+  of its own k-mer and the summary tokens before it in its window, including
+  the boundary summary carried over from the previous window; a summary token
+  sees its own k-mer, the earlier summaries of its window and that carried
+  boundary.  Nothing else of earlier windows is visible.  Readings taken where
+  the section is silent: the carried boundary is the last summary token of the
+  previous window of the same sequence (the last retained cache row); a token
+  sees itself; a window with k_w = 0 has no summaries and is a single k-mer
+  (plain causal attention inside it, plus the carried boundary).
+  kmer_local_stream_visibility states the rule over a whole augmented sequence
+  (masked-parallel form); kmer_local_window_visibility states it over one
+  window's [cache ; window] keys, the form the kernels take.
+
 All matrix products are NumPy float64 matmuls; masking is an explicit boolean
 matrix; the softmax is the definition (shift by the row max, exponentiate,
 normalise).  Inputs are float arrays holding the exact values the kernels
@@ -182,6 +196,100 @@ def dense_causal(q, k, v, scale=None):
     if scale is None:
         scale = default_scale(D)
     vis = np.tril(np.ones((n, n), bool))
+    o = np.empty((n, H, D), np.float64)
+    lse = np.empty((n, H), np.float64)
+    for h in range(H):
+        g = h // (H // Hkv)
+        o[:, h], lse[:, h], _ = attend(q[:, h], k[:, g], v[:, g], vis, scale)
+    return o, lse
+
+
+# ---------------------------------------------------------------- k-mer-local
+
+def kmer_local_stream_visibility(layout, b: int):
+    """Section 3.2 rule over the augmented stream of sequence b: u is visible to
+    t iff u <= t and u lies in t's window and (u is in t's k-mer or u is a
+    summary token), or u is the carried boundary of t's window (the last summary
+    token of the previous window of the sequence).  The k-mer of a token is the
+    one its closing summary ends (tok_kmer); k_w = 0 makes the window one k-mer."""
+    t0, t1 = int(layout["cu_tokens"][b]), int(layout["cu_tokens"][b + 1])
+    n = t1 - t0
+    win = layout["tok_win"][t0:t1]
+    kmer = layout["tok_kmer"][t0:t1]
+    is_sum = layout["tok_kind"][t0:t1] == SUMMARY
+    vis = np.zeros((n, n), bool)
+    for t in range(n):
+        # the carried boundary: the last summary token of an earlier window
+        boundary = -1
+        for u in range(t):
+            if win[u] != win[t] and is_sum[u]:
+                boundary = u
+        for u in range(t + 1):
+            if win[u] == win[t]:
+                vis[t, u] = kmer[u] == kmer[t] or is_sum[u]
+            elif u == boundary:
+                vis[t, u] = True
+    return vis
+
+
+def kmer_local_window_visibility(layout, w: int):
+    """The same rule for window w over keys [cache rows 0..C_w-1 ; window rows]:
+    cache row r is visible only if it is the last one (r = C_w - 1, the carried
+    boundary); window row u is visible to window query i iff u <= i and (u is in
+    i's k-mer or u is a summary)."""
+    t0 = int(layout["win_tok_off"][w])
+    T = int(layout["win_ntok"][w])
+    C = int(layout["win_cache_off"][w])
+    kmer = layout["tok_kmer"][t0:t0 + T]
+    is_sum = layout["tok_kind"][t0:t0 + T] == SUMMARY
+    vis = np.zeros((T, C + T), bool)
+    if C > 0:
+        vis[:, C - 1] = True
+    i = np.arange(T)[:, None]
+    u = np.arange(T)[None, :]
+    vis[:, C:] = (u <= i) & ((kmer[None, :] == kmer[:, None]) | is_sum[None, :])
+    return vis
+
+
+def window_attention_masked(q_win, k_win, v_win, cache_k, cache_v, visible, scale=None):
+    """window_attention with an explicit visibility matrix over [cache ; window]."""
+    T, H, D = q_win.shape
+    Hkv = k_win.shape[1]
+    if H % Hkv:
+        raise ValueError("heads must be a multiple of kv heads")
+    if scale is None:
+        scale = default_scale(D)
+    o = np.empty((T, H, D), np.float64)
+    lse = np.empty((T, H), np.float64)
+    for h in range(H):
+        g = h // (H // Hkv)
+        keys = np.concatenate([cache_k[:, g, :], k_win[:, g, :]], axis=0)
+        vals = np.concatenate([cache_v[:, g, :], v_win[:, g, :]], axis=0)
+        o[:, h, :], lse[:, h], _ = attend(q_win[:, h, :], keys, vals, visible, scale)
+    return o, lse
+
+
+def kmer_local_window(layout, w: int, q, k, v, scale=None):
+    """k-mer-local attention outputs of window w from arrays indexed by global
+    token (cache rows are the earlier windows' summary tokens, as in C(t))."""
+    t0 = int(layout["win_tok_off"][w])
+    T = int(layout["win_ntok"][w])
+    idx = cache_token_indices(layout, w)
+    q, k, v = np.asarray(q), np.asarray(k), np.asarray(v)
+    return window_attention_masked(q[t0:t0 + T], k[t0:t0 + T], v[t0:t0 + T], k[idx], v[idx],
+                                   kmer_local_window_visibility(layout, w), scale)
+
+
+def kmer_local_masked_parallel(layout, q, k, v, b: int, scale=None):
+    """k-mer-local attention over the whole augmented sequence b under the
+    stream-domain rule.  Returns O, LSE of its tokens."""
+    t0, t1 = int(layout["cu_tokens"][b]), int(layout["cu_tokens"][b + 1])
+    q, k, v = np.asarray(q)[t0:t1], np.asarray(k)[t0:t1], np.asarray(v)[t0:t1]
+    n, H, D = q.shape
+    Hkv = k.shape[1]
+    if scale is None:
+        scale = default_scale(D)
+    vis = kmer_local_stream_visibility(layout, b)
     o = np.empty((n, H, D), np.float64)
     lse = np.empty((n, H), np.float64)
     for h in range(H):

@@ -18,6 +18,7 @@ import oracle.decode
 import oracle.layout
 import test_oracle_attention as TA
 import test_oracle_decode as TD
+import test_oracle_kmer_local as TK
 import test_oracle_layout as TL
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -59,6 +60,16 @@ def _attention_pins():
     TA.test_compaction_keeps_summary_rows_in_order(0)
 
 
+def _kmer_local_pins():
+    for seed in range(4):
+        TK.test_stream_form_equals_window_form(seed)
+        TK.test_zero_keys_one_hot_values_spell_out_the_visible_set(seed)
+        TK.test_earlier_rows_and_other_kmer_bases_are_invisible(seed)
+        TK.test_first_kmer_is_textbook_causal(seed)
+        TK.test_one_kmer_per_window_is_causal_plus_boundary(seed)
+    TK.test_zero_kmer_single_window_is_dense_causal()
+
+
 def _decode_pins():
     TD.test_decode_from_empty_equals_prefill(37, 10, 3)
     TD.test_decode_from_empty_equals_prefill(25, 7, 7)
@@ -74,10 +85,15 @@ ATTENTION_MUTATIONS = [
     ("scale dropped", "s = scale * (q @ keys.T)", "s = (q @ keys.T)"),
     ("no max shift in lse", "lse = (m + np.log(l))[:, 0]", "lse = np.log(l)[:, 0]"),
     ("values of the wrong rows", "o = p @ values", "o = p @ values[::-1]"),
-    ("kv head of the wrong group", "g = h // (H // Hkv)\n        keys", "g = h % Hkv\n        keys"),
+    ("kv head of the wrong group",
+     "vis = window_visibility(T, C)\n    o = np.empty((T, H, D), np.float64)\n    lse = np.empty((T, H), np.float64)\n"
+     "    for h in range(H):\n        g = h // (H // Hkv)",
+     "vis = window_visibility(T, C)\n    o = np.empty((T, H, D), np.float64)\n    lse = np.empty((T, H), np.float64)\n"
+     "    for h in range(H):\n        g = h % Hkv"),
     ("ordinary rows kept", "keep = np.nonzero(layout[\"tok_kind\"][t0:t1] == SUMMARY)[0] + t0",
      "keep = np.arange(t0, t1)"),
-    ("masked-parallel without summaries", "| is_sum[None, :])", ")"),
+    ("masked-parallel without summaries", "((win[None, :] == win[:, None]) | is_sum[None, :])",
+     "((win[None, :] == win[:, None]))"),
     ("cache offset off by one", "first:first + int(layout[\"win_cache_off\"][w])]",
      "first:first + int(layout[\"win_cache_off\"][w]) + 1]"),
 ]
@@ -97,6 +113,18 @@ DECODE_MUTATIONS = [
     ("window never reset", "self.win_k, self.win_v = [], []", "pass"),
     ("summary into window buffer", "self.cache_k.append(np.asarray(k_new))",
      "self.win_k.append(np.asarray(k_new))"),
+]
+
+
+KMER_LOCAL_MUTATIONS = [
+    ("boundary row dropped", "        vis[:, C - 1] = True\n", "        vis[:, C - 1] = False\n"),
+    ("every earlier summary visible", "            elif u == boundary:", "            elif is_sum[u]:"),
+    ("boundary from the first window", "                boundary = u\n",
+     "                boundary = u if boundary < 0 else boundary\n"),
+    ("token does not see itself", "vis[:, C:] = (u <= i) & (", "vis[:, C:] = (u < i) & ("),
+    ("bases of earlier k-mers visible", "((kmer[None, :] == kmer[:, None]) | is_sum[None, :])",
+     "((kmer[None, :] <= kmer[:, None]) | is_sum[None, :])"),
+    ("later summaries visible", "vis[:, C:] = (u <= i) & (", "vis[:, C:] = (u >= 0) & ("),
 ]
 
 
@@ -125,7 +153,14 @@ def test_decode_mutations_are_caught(monkeypatch, name, old, new):
     _expect_caught(monkeypatch, _decode_pins, [(TD, "DecodeSequence", mut.DecodeSequence)])
 
 
+@pytest.mark.parametrize("name,old,new", KMER_LOCAL_MUTATIONS, ids=[m[0] for m in KMER_LOCAL_MUTATIONS])
+def test_kmer_local_mutations_are_caught(monkeypatch, name, old, new):
+    mut = _mutant(oracle.attention, old, new)
+    _expect_caught(monkeypatch, _kmer_local_pins, [(TK, "A", mut)])
+
+
 def test_unmutated_pins_pass():
     _layout_pins()
     _attention_pins()
     _decode_pins()
+    _kmer_local_pins()
