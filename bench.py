@@ -17,7 +17,8 @@ Also reported on the same JSON line:
   cpu_baseline  the float64 oracle on a bounded sample of the same workload
                 (whole windows, all heads), extrapolated by visible pairs
   secondary     compaction and decode (batch 16 at ~1 Mb) HBM rates, the dense
-                32 kb causal point, and streaming (one window per call) prefill
+                32 kb causal point, streaming (one window per call) prefill, and
+                the same 1 Mb prefill under the k-mer-local mask (HBM-bound)
 """
 
 from __future__ import annotations
@@ -59,6 +60,23 @@ def visible_pairs(win_ntok, win_cache_off):
     T = win_ntok.astype(np.int64)
     C = win_cache_off.astype(np.int64)
     return int((T * C + T * (T + 1) // 2).sum())
+
+
+def kmer_local_pairs(win_ntok, win_cache_off, win_kmer):
+    """Query-key pairs the k-mer-local mask admits, in closed form per window:
+    a token at offset p of k-mer g sees p + 1 tokens of its k-mer, the g earlier
+    summaries of its window and the carried boundary (when C_w > 0)."""
+    T = np.asarray(win_ntok, np.int64)
+    bnd = (np.asarray(win_cache_off, np.int64) > 0).astype(np.int64)
+    k = np.broadcast_to(np.asarray(win_kmer, np.int64), T.shape)
+    dense = T * (T + 1) // 2 + T * bnd                                    # k = 0: one k-mer
+    kp = np.maximum(k, 0) + 1
+    B = np.where(k > 0, (T + kp - 1) // kp, 1)
+    nf = B - 1                                                            # full k-mers
+    last = T - nf * kp
+    full = nf * kp * (kp + 1) // 2 + kp * (nf * (nf - 1) // 2 + nf * bnd)
+    tail = last * (last + 1) // 2 + last * (nf + bnd)
+    return int(np.where(k > 0, full + tail, dense).sum())
 
 
 class Timer:
@@ -282,6 +300,30 @@ def secondary_dense(torch, F, fw, reps=3):
             "dense_1mb_extrapolated_s": ms * 1e-3 * (1e6 / n) ** 2}
 
 
+def secondary_kmer_local(torch, F, fw, s, timer, reps=5):
+    """The same 1 Mb layout under the k-mer-local mask (Section 3.2 rule): every
+    window in one launch.  Bound by HBM: Q, K, V and O cross it once."""
+    mask = F.FOCUS_MASK_KMER_LOCAL
+    F.focus_window_attn(s["lay"], s["q"], s["k"], s["v"], s["ck"], s["cv"], o=s["o"], lse=s["lse"], mask=mask)
+    for _ in range(reps):
+        a = timer.span("kmer_local")
+        a[0].record()
+        F.focus_window_attn(s["lay"], s["q"], s["k"], s["v"], s["ck"], s["cv"], o=s["o"], lse=s["lse"], mask=mask)
+        a[1].record()
+    torch.cuda.synchronize()
+    ms = timer.mean_ms("kmer_local")
+    w, tot = s["w"], s["totals"]
+    lay = s["lay"]
+    pairs = kmer_local_pairs(lay["win_ntok"].cpu().numpy(), lay["win_cache_off"].cpu().numpy(), fw.kmer_draw(w))
+    flops = 4 * w.head_dim * w.heads * pairs
+    per_tok = w.heads * w.head_dim * 2 * 2 + 2 * w.kv_heads * w.head_dim * 2 + w.heads * 4   # q, o, k, v, lse
+    nbytes = tot.n_tokens * per_tok + tot.n_windows * 2 * w.kv_heads * w.head_dim * 2     # + boundary rows
+    return {"workload": f"{w.name} under FOCUS_MASK_KMER_LOCAL, all windows in one launch", "ms": ms,
+            "nt_per_s": w.seq_nt * w.batch / (ms * 1e-3), "visible_pairs_per_head": pairs,
+            "tflops": flops / ms / 1e9, "bytes": nbytes, "GBps": nbytes / ms / 1e6,
+            "bound": "hbm", "frac_hbm": nbytes / (ms * 1e-3) / PEAK_HBM}
+
+
 def secondary_streaming(torch, F, s, n_windows=200):
     """Streaming prefill: one window per call (last n_windows windows)."""
     lay = s["lay"]
@@ -385,6 +427,8 @@ def main():
         sec = {"compaction_1mb": secondary_compaction(torch, F, s, timer)}
         log("secondary: streaming")
         sec["streaming_1mb"] = secondary_streaming(torch, F, s)
+        log("secondary: k-mer-local mask")
+        sec["kmer_local_1mb"] = secondary_kmer_local(torch, F, fw, s, timer)
         if not args.no_cpu_baseline:
             log("cpu baseline (oracle)")
             result["cpu_baseline"] = cpu_baseline(torch, s, args.cpu_budget)

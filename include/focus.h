@@ -49,7 +49,7 @@
 extern "C" {
 #endif
 
-#define FOCUS_ABI_VERSION 1
+#define FOCUS_ABI_VERSION 2
 
 typedef int32_t focus_status;
 enum {
@@ -70,8 +70,12 @@ typedef enum { FOCUS_BF16 = 0, FOCUS_F32 = 1 } focus_dtype;
  * FOCUS_MASK_CT: the set C(t) of Appendix A.1 ("Objective and visibility"):
  *   a token sees every earlier-or-equal token of its own window and every
  *   retained summary of the earlier windows of its sequence.
- * FOCUS_MASK_KMER_LOCAL: the stricter Section 3.2 rule (a base sees only its own
- *   k-mer and earlier summaries of its window); returns FOCUS_E_UNSUPPORTED. */
+ * FOCUS_MASK_KMER_LOCAL: the stricter rule of Section 3.2 ("Visibility and
+ *   summarization rule"): a token sees the earlier-or-equal tokens of its own
+ *   k-mer (a summary closes its k-mer), the earlier summaries of its own window
+ *   and the boundary summary carried over from the previous window, which is
+ *   the last retained cache row C_w - 1.  Nothing else of earlier windows is
+ *   visible.  A window with k = 0 is one k-mer (causal inside the window). */
 typedef enum { FOCUS_MASK_CT = 0, FOCUS_MASK_KMER_LOCAL = 1 } focus_mask;
 
 /* tok_kind values */
@@ -219,6 +223,8 @@ focus_status focus_compact_kv(const focus_compact_desc* d, focus_stream_t stream
  * row i in [0, T_w) (global token t = win_tok_off[w] + i):
  *     keys     = [cache_k[b, 0:C_w, g] ; k[window rows, g]],  g = h / (H / H_kv)
  *     visible  = every cache row, and window rows u <= i      (FOCUS_MASK_CT)
+ *              = cache row C_w - 1, and window rows u <= i that are summaries
+ *                or lie in row i's k-mer                   (FOCUS_MASK_KMER_LOCAL)
  *     o[t, h]  = softmax(scale * q[t, h] . keys^T over visible) . values
  *     lse[t,h] = log sum_visible exp(scale * q[t, h] . key)
  * (Appendix A eq. focus-attn with the visibility set C(t) of A.1.)  The cache
@@ -229,6 +235,10 @@ focus_status focus_compact_kv(const focus_compact_desc* d, focus_stream_t stream
  * with the largest C_w + T_w first.
  *   softmax_scale <= 0 selects 1/sqrt(head_dim).
  *   Supported: head_dim 64 or 128, bf16 or f32, n_heads a multiple of n_kv_heads.
+ * FOCUS_MASK_KMER_LOCAL reads the window's own summaries from its window rows
+ * (k-mer j of a window with cadence k spans window rows [j (k+1), j (k+1) + k],
+ * its summary last, as focus_layout places them) and needs each window's k:
+ * win_kmer (the per-window array given to focus_layout) or kmer_uniform.
  */
 typedef struct {
   focus_layout_totals totals;
@@ -239,7 +249,8 @@ typedef struct {
   float softmax_scale;
   int32_t mask;                 /* focus_mask                                */
   int32_t batch;
-  int32_t reserved;
+  int32_t kmer_uniform;         /* k of every window if win_kmer is NULL
+                                   (FOCUS_MASK_KMER_LOCAL only; >= 0)        */
   int64_t n_win;                /* entries of win_ids (ignored if NULL)      */
   const int32_t* win_ids;       /* [device] or NULL = all windows, in the
                                    order last window first                   */
@@ -247,6 +258,8 @@ typedef struct {
   const int32_t* win_ntok;
   const int32_t* win_cache_off;
   const int64_t* win_tok_off;
+  const int32_t* win_kmer;      /* [device][n_windows] k per window, or NULL
+                                   (FOCUS_MASK_KMER_LOCAL only)              */
   const void* q;                /* [qkv_rows, n_heads, head_dim]             */
   const void* k;                /* [qkv_rows, n_kv_heads, head_dim]          */
   const void* v;                /*   row r = global token qkv_tok_base + r   */

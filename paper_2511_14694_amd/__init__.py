@@ -91,6 +91,8 @@ class Layout:
     batch: int
     window_nt: int
     arrays: Dict[str, torch.Tensor] = field(default_factory=dict)
+    kmer: Optional[torch.Tensor] = None   # per-window k given to focus_layout (device), or None
+    kmer_uniform: int = 0                 # k of every window when kmer is None
 
     def __getitem__(self, name):
         return self.arrays[name]
@@ -136,7 +138,7 @@ def focus_layout(totals: LayoutTotals, seq_nt, window_nt: int, kmer=None, kmer_u
     for f, t in arrays.items():
         setattr(d, f, _ptr(t))
     check("focus_layout", lib().focus_layout(C.byref(d), _stream(stream, dev)))
-    return Layout(totals, B, int(window_nt), arrays)
+    return Layout(totals, B, int(window_nt), arrays, km, int(kmer_uniform))
 
 
 def focus_compact_kv(lay: Layout, k, v, cache_k, cache_v, cache_len=None, win_ids=None,
@@ -173,6 +175,8 @@ def _attn_desc(lay, q, k, v, cache_k, cache_v, o, lse, win_ids, qkv_tok_base, so
     d.softmax_scale = float(softmax_scale)
     d.mask = int(mask)
     d.batch = lay.batch
+    d.kmer_uniform = int(lay.kmer_uniform)
+    d.win_kmer = _ptr(lay.kmer)
     d.n_win = 0 if win_ids is None else win_ids.numel()
     d.win_ids = _ptr(win_ids)
     for f in ("win_seq", "win_ntok", "win_cache_off", "win_tok_off"):

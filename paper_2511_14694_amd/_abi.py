@@ -52,8 +52,9 @@ class CompactDesc(C.Structure):
 class AttnDesc(C.Structure):
     _fields_ = [("totals", LayoutTotals), ("dtype", i32), ("n_heads", i32), ("n_kv_heads", i32),
                 ("head_dim", i32), ("softmax_scale", f32), ("mask", i32), ("batch", i32),
-                ("reserved", i32), ("n_win", i64), ("win_ids", p),
+                ("kmer_uniform", i32), ("n_win", i64), ("win_ids", p),
                 ("win_seq", p), ("win_ntok", p), ("win_cache_off", p), ("win_tok_off", p),
+                ("win_kmer", p),
                 ("q", p), ("k", p), ("v", p), ("qkv_tok_base", i64), ("qkv_rows", i64),
                 ("cache_k", p), ("cache_v", p), ("cache_cap", i64), ("o", p), ("lse", p),
                 ("workspace", p), ("workspace_bytes", sz), ("err", p)]

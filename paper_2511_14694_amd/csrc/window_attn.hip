@@ -1,13 +1,22 @@
 // Window attention over [retained summary cache ; window] (focus_window_attn).
 //
-// For window w of sequence b, query row i (0 <= i < T_w) of head h attends to
-// every cache row j < C_w and to window rows u <= i: the visibility set C(t) of
-// Appendix A.1, which is also the mask of the masked-parallel form (A.1,
-// "Cross-window consistency").  One launch may cover any set of windows of any
-// sequences; each window only reads the cache rows its predecessors retained.
+// C(t) mask: for window w of sequence b, query row i (0 <= i < T_w) of head h
+// attends to every cache row j < C_w and to window rows u <= i: the visibility
+// set C(t) of Appendix A.1, which is also the mask of the masked-parallel form
+// (A.1, "Cross-window consistency").  One launch may cover any set of windows
+// of any sequences; each window only reads the cache rows its predecessors
+// retained.
 //
-// bf16 path (the hot one), one workgroup = 4 waves = 128 query rows of one
-// (window, head), keys streamed in tiles of 64 through LDS, double-buffered:
+// k-mer-local mask (Section 3.2, "Visibility and summarization rule"): query
+// row i sees the earlier-or-equal rows of its own k-mer, the earlier summaries
+// of its window and the carried boundary (cache row C_w - 1).  The keys are
+// visited as a gathered summary list [boundary ; the window's summaries] and
+// then only the window tiles that hold the block's k-mers; a two-sided mask
+// keeps each row's own k-mer.
+//
+// bf16 path (the hot one): one workgroup = 8 waves (4 under the k-mer-local
+// mask) = 32 query rows per wave of one (window, head); keys stream in tiles
+// of 64 through LDS, double-buffered, copied global -> LDS directly:
 //   S^T = K Q^T   v_mfma_f32_32x32x16_bf16: each lane ends up holding one
 //                 query's scores for 16 keys of a 32-key block, so the row
 //                 max / row sum are lane-local plus one exchange with lane^32;
@@ -44,8 +53,12 @@ constexpr float kLazy = 8.0f;       // rescale when the max grows by > 2^8
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 typedef __attribute__((address_space(3))) void lds_void;
 
-// Waves per workgroup of the bf16 kernel (each wave owns 32 query rows).
+// Waves per workgroup of the bf16 kernel (each wave owns 32 query rows):
+// eight under C(t), where a workgroup streams thousands of keys; four under the
+// k-mer-local mask, where it visits a handful of tiles and two workgroups per
+// CU hide each other's start-up.
 constexpr int kBf16Waves = 8;
+constexpr int kBf16WavesKL = 4;
 
 struct Item {
   int64_t list_idx;
@@ -105,7 +118,7 @@ __device__ inline int v_off(int r, int byte) {
   return r * (D * 2) + ((((byte >> 6) ^ f)) << 6) + (byte & 63);
 }
 
-template <int D, int W>
+template <int D, int W, bool KL>
 __global__ __launch_bounds__(64 * W, 2) void attn_bf16(focus_attn_desc d, float sc, int64_t n_pairs, int QT) {
   using C = Cfg<D, W>;
   // Two K and two V tile buffers as separate arrays, referenced statically by
@@ -135,16 +148,40 @@ __global__ __launch_bounds__(64 * W, 2) void attn_bf16(focus_attn_desc d, float 
   const int H = d.n_heads, Hkv = d.n_kv_heads, h = it.h;
   const int hk = h / (H / Hkv);
   const int nwk = min(T, q0 + C::kBQ);  // window keys any query of this tile can see
-  // Keys are visited as nct tiles of cache rows [0, Cw) followed by nwt tiles
-  // of window rows [0, nwk); only the last tile of each phase is partial.
-  const int nct = (Cw + C::kBK - 1) / C::kBK;
-  const int nwt = (nwk + C::kBK - 1) / C::kBK;
+  // C(t): keys are visited as nct tiles of cache rows [0, Cw) followed by nwt
+  // tiles of window rows [0, nwk); only the last tile of each phase is partial.
+  // k-mer-local: the first nct tiles hold the summary list [carried boundary
+  // (cache row Cw - 1) ; the window's nsum summaries], gathered row by row;
+  // the window tiles start at tile tw0, the one holding the first row of the
+  // k-mer of the block's first query.
+  int kw = 0, nsum = 0, tw0 = 0;
+  if constexpr (KL) {
+    kw = d.win_kmer ? d.win_kmer[gw] : d.kmer_uniform;
+    if (kw < 0) {
+      if (tid == 0) focus::raise_err(d.err, FOCUS_ERR_BOUNDS);
+      return;
+    }
+    nsum = kw > 0 ? (T + kw) / (kw + 1) : 0;
+    tw0 = kw > 0 ? (q0 / (kw + 1)) * (kw + 1) / C::kBK : 0;
+  }
+  const int nct = KL ? (nsum + C::kBK) / C::kBK : (Cw + C::kBK - 1) / C::kBK;
+  const int nwt = (nwk + C::kBK - 1) / C::kBK - tw0;
   const int ntiles = nct + nwt;
 
   const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, g = lane >> 5;
   const int qi = q0 + wave * 32 + l32;  // this lane's query row inside the window
   const int wq_lo = q0 + wave * 32, wq_hi = wq_lo + 31;
   const bool wave_live = wq_lo < T;
+  // k-mer-local: this lane's k-mer index jq inside the window and that
+  // k-mer's first row qlo; klo_w: first row of the wave's first k-mer.
+  int jq = 0, qlo = 0, klo_w = 0;
+  if constexpr (KL) {
+    if (kw > 0) {
+      jq = qi / (kw + 1);
+      qlo = jq * (kw + 1);
+      klo_w = wq_lo / (kw + 1) * (kw + 1);
+    }
+  }
 
   // Q^T as the B operand: lane holds query l32, head_dim [16s + 8g, 16s + 8g + 8).
   bf16x8 qf[C::kKsteps];
@@ -187,8 +224,31 @@ __global__ __launch_bounds__(64 * W, 2) void attn_bf16(focus_attn_desc d, float 
 
   // Tile x lives in buffers x & 1.
   auto issue_tile = [&](int t, char* kbuf, char* vbuf) {
+    if constexpr (KL) {
+      if (t < nct) {
+        // Summary-list entry R = 64 t + r: R = 0 is the carried boundary, R >= 1
+        // the window's summary R - 1 at window row R (k + 1) - 1 (the last one at
+        // T - 1).  Rows past the list repeat its last entry (masked).
+        char* kl = kbuf + wave * kDma * 1024;
+        char* vl = vbuf + wave * kDma * 1024;
+#pragma unroll
+        for (int i = 0; i < kDma; ++i) {
+          const int r = (wave * kDma + i) * kRPK + lane / C::kCh16;
+          const int R = min(t * C::kBK + r, nsum);
+          const bool boundary = R == 0 && Cw > 0;
+          const int wrow = R == 0 ? 0 : min(R * (kw + 1) - 1, T - 1);
+          const char* kp = boundary ? kcache + (int64_t)(Cw - 1) * row_bytes : kwin + (int64_t)wrow * row_bytes;
+          const char* vp = boundary ? vcache + (int64_t)(Cw - 1) * row_bytes : vwin + (int64_t)wrow * row_bytes;
+          const char* ks = kp + kchunk[i];
+          const char* vs = vp + vchunk[i];
+          __builtin_amdgcn_global_load_lds(ks, (lds_void*)(kl + i * 1024), 16, 0, 0);
+          __builtin_amdgcn_global_load_lds(vs, (lds_void*)(vl + i * 1024), 16, 0, 0);
+        }
+        return;
+      }
+    }
     const bool in_cache = t < nct;
-    const int row0 = in_cache ? t * C::kBK : (t - nct) * C::kBK;
+    const int row0 = in_cache ? t * C::kBK : (t - nct + tw0) * C::kBK;
     const int nvalid = (in_cache ? Cw : nwk) - row0;
     const char* kb = (in_cache ? kcache : kwin) + (int64_t)row0 * row_bytes;
     const char* vb = (in_cache ? vcache : vwin) + (int64_t)row0 * row_bytes;
@@ -217,11 +277,13 @@ __global__ __launch_bounds__(64 * W, 2) void attn_bf16(focus_attn_desc d, float 
   auto compute_tile = [&](int t, const char* kl, const char* vl) {
     // Key kk of the tile (0..63) is visible to this lane's query iff kk <= lim:
     // cache tiles hide only rows past Cw, window tiles are causal.
-    const bool in_cache = t < nct;
-    const int row0 = in_cache ? t * C::kBK : (t - nct) * C::kBK;
-    const bool live = wave_live && (in_cache || row0 <= wq_hi);
-    const bool need_mask = in_cache ? row0 + C::kBK > Cw : row0 + C::kBK - 1 > wq_lo;
-    const int lim = in_cache ? Cw - row0 - 1 : qi - row0;
+    const bool in_cache = t < nct;  // (k-mer-local: the summary list)
+    const int row0 = in_cache ? t * C::kBK : (t - nct + tw0) * C::kBK;
+    const bool live = wave_live && (in_cache || (row0 <= wq_hi && (!KL || row0 + C::kBK > klo_w)));
+    const bool need_mask = KL || (in_cache ? row0 + C::kBK > Cw : row0 + C::kBK - 1 > wq_lo);
+    // visible tile keys: lo <= kk <= lim (lo only for k-mer-local)
+    const int lim = KL ? (in_cache ? jq - row0 : qi - row0) : (in_cache ? Cw - row0 - 1 : qi - row0);
+    const int lo = KL ? (in_cache ? (Cw > 0 ? 0 : 1) - row0 : qlo - row0) : 0;
     if (live) {
       f32x16 sacc[2];
 #pragma unroll
@@ -237,12 +299,14 @@ __global__ __launch_bounds__(64 * W, 2) void attn_bf16(focus_attn_desc d, float 
       }
       // sacc[st][v] = score of query qi with tile key 32 st + 8 (v/4) + 4 g + v%4
       if (need_mask) {
-        const int lim_g = lim - 4 * g;
+        const int lim_g = lim - 4 * g, lo_g = lo - 4 * g;
 #pragma unroll
         for (int st = 0; st < 2; ++st)
 #pragma unroll
-          for (int v = 0; v < 16; ++v)
-            if (st * 32 + (v >> 2) * 8 + (v & 3) > lim_g) sacc[st][v] = -INFINITY;
+          for (int v = 0; v < 16; ++v) {
+            const int kk = st * 32 + (v >> 2) * 8 + (v & 3);
+            if (kk > lim_g || (KL && kk < lo_g)) sacc[st][v] = -INFINITY;
+          }
       }
       float mx = -INFINITY;
 #pragma unroll
@@ -328,7 +392,7 @@ __global__ __launch_bounds__(64 * W, 2) void attn_bf16(focus_attn_desc d, float 
 
 // ----------------------------------------------------------------- f32 VALU
 
-template <int D>
+template <int D, bool KL>
 __global__ __launch_bounds__(256) void attn_f32(focus_attn_desc d, float sc, int64_t n_pairs, int QT) {
   constexpr int kBQ = 64, kBK = 32, kF4 = D / 4, kPer = D / 16;  // float4 per row / per lane
   __shared__ float4 ks[kBK][kF4];
@@ -356,6 +420,24 @@ __global__ __launch_bounds__(256) void attn_f32(focus_attn_desc d, float sc, int
   const int hk = h / (H / Hkv);
   const int nkeys = Cw + min(T, q0 + kBQ);
   const int qi = q0 + (tid >> 2), sub = tid & 3;
+  int kw = 0;
+  if constexpr (KL) {
+    kw = d.win_kmer ? d.win_kmer[gw] : d.kmer_uniform;
+    if (kw < 0) {
+      if (tid == 0) focus::raise_err(d.err, FOCUS_ERR_BOUNDS);
+      return;
+    }
+  }
+  // key j of [cache ; window] is visible to this lane's query
+  auto visible = [&](int j) {
+    if (!KL) return j < Cw || j - Cw <= qi;
+    if (j < Cw) return j == Cw - 1;  // only the carried boundary
+    const int u = j - Cw;
+    if (u > qi) return false;
+    if (kw == 0) return true;
+    const bool summary = u % (kw + 1) == kw || u == T - 1;
+    return summary || u / (kw + 1) == qi / (kw + 1);
+  };
   const int64_t row_f4 = (int64_t)Hkv * kF4;
 
   float4 qv[kPer], ov[kPer];
@@ -402,7 +484,7 @@ __global__ __launch_bounds__(256) void attn_f32(focus_attn_desc d, float sc, int
       }
       s = focus::sum4(s) * sc;
       const int j = j0 + kk;
-      if (j < Cw || j - Cw <= qi) {
+      if (visible(j)) {
         const float m_new = fmaxf(m, s);
         const float corr = __builtin_amdgcn_exp2f(m - m_new);
         const float p = __builtin_amdgcn_exp2f(s - m_new);
@@ -439,8 +521,8 @@ extern "C" size_t focus_window_attn_workspace(const focus_attn_desc* d) {
 extern "C" focus_status focus_window_attn(const focus_attn_desc* d, focus_stream_t stream) {
   if (!d) return FOCUS_E_NULL;
   if (d->dtype != FOCUS_BF16 && d->dtype != FOCUS_F32) return FOCUS_E_DTYPE;
-  if (d->mask == FOCUS_MASK_KMER_LOCAL) return FOCUS_E_UNSUPPORTED;
-  if (d->mask != FOCUS_MASK_CT) return FOCUS_E_ARG;
+  if (d->mask != FOCUS_MASK_CT && d->mask != FOCUS_MASK_KMER_LOCAL) return FOCUS_E_ARG;
+  if (d->mask == FOCUS_MASK_KMER_LOCAL && !d->win_kmer && d->kmer_uniform < 0) return FOCUS_E_ARG;
   if (d->n_heads <= 0 || d->n_kv_heads <= 0 || d->batch < 0 || d->cache_cap < 0 ||
       d->qkv_rows < 0 || (d->win_ids && d->n_win < 0) || !(d->softmax_scale == d->softmax_scale))
     return FOCUS_E_ARG;
@@ -464,23 +546,29 @@ extern "C" focus_status focus_window_attn(const focus_attn_desc* d, focus_stream
   const float scale = d->softmax_scale > 0.f ? d->softmax_scale : 1.0f / sqrtf((float)d->head_dim);
   const float sc = scale * kLog2e;
   const int64_t n_pairs = nwl * d->n_heads;
-  const int bq = d->dtype == FOCUS_BF16 ? 32 * kBf16Waves : 64;
-  const int threads = d->dtype == FOCUS_BF16 ? 64 * kBf16Waves : 256;
+  const bool kl = d->mask == FOCUS_MASK_KMER_LOCAL;
+  const int waves = kl ? kBf16WavesKL : kBf16Waves;
+  const int bq = d->dtype == FOCUS_BF16 ? 32 * waves : 64;
+  const int threads = d->dtype == FOCUS_BF16 ? 64 * waves : 256;
   const int64_t qt = focus::ceil_div(t.max_window_tokens, bq);
   const int64_t blocks = focus::ceil_div(n_pairs, focus::kXcds) * focus::kXcds * qt;
   if (blocks * threads >= ((int64_t)1 << 32) || qt > INT32_MAX) return FOCUS_E_SHAPE;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const dim3 grid((uint32_t)blocks), block(threads);
+#define FOCUS_ATTN_LAUNCH(KERNEL) hipLaunchKernelGGL(KERNEL, grid, block, 0, s, *d, sc, n_pairs, (int)qt)
   if (d->dtype == FOCUS_BF16) {
-    if (d->head_dim == 128)
-      hipLaunchKernelGGL((attn_bf16<128, kBf16Waves>), grid, block, 0, s, *d, sc, n_pairs, (int)qt);
-    else
-      hipLaunchKernelGGL((attn_bf16<64, kBf16Waves>), grid, block, 0, s, *d, sc, n_pairs, (int)qt);
+    if (d->head_dim == 128) {
+      if (kl) FOCUS_ATTN_LAUNCH((attn_bf16<128, kBf16WavesKL, true>)); else FOCUS_ATTN_LAUNCH((attn_bf16<128, kBf16Waves, false>));
+    } else {
+      if (kl) FOCUS_ATTN_LAUNCH((attn_bf16<64, kBf16WavesKL, true>)); else FOCUS_ATTN_LAUNCH((attn_bf16<64, kBf16Waves, false>));
+    }
   } else {
-    if (d->head_dim == 128)
-      hipLaunchKernelGGL(attn_f32<128>, grid, block, 0, s, *d, sc, n_pairs, (int)qt);
-    else
-      hipLaunchKernelGGL(attn_f32<64>, grid, block, 0, s, *d, sc, n_pairs, (int)qt);
+    if (d->head_dim == 128) {
+      if (kl) FOCUS_ATTN_LAUNCH((attn_f32<128, true>)); else FOCUS_ATTN_LAUNCH((attn_f32<128, false>));
+    } else {
+      if (kl) FOCUS_ATTN_LAUNCH((attn_f32<64, true>)); else FOCUS_ATTN_LAUNCH((attn_f32<64, false>));
+    }
   }
+#undef FOCUS_ATTN_LAUNCH
   return focus::launch_status();
 }

@@ -41,7 +41,7 @@ def test_struct_mirrors_and_version():
     for i, st in enumerate(_abi.STRUCTS):
         assert lib.focus_struct_size(i) == C.sizeof(st)
     assert lib.focus_struct_size(99) == -1
-    assert F.focus_abi_version() == 1
+    assert F.focus_abi_version() == 2
     assert lib.focus_status_str(0) == b"ok"
     assert lib.focus_status_str(5) == b"unsupported configuration"
 
@@ -118,7 +118,7 @@ def _attn_ok():
 @pytest.mark.parametrize("mutate,status", [
     (lambda d: setattr(d, "dtype", 7), 4),
     (lambda d: setattr(d, "head_dim", 96), 5),
-    (lambda d: setattr(d, "mask", 1), 5),
+    (lambda d: setattr(d, "kmer_uniform", -1) or setattr(d, "mask", 1), 2),
     (lambda d: setattr(d, "mask", 9), 2),
     (lambda d: setattr(d, "n_kv_heads", 3), 3),
     (lambda d: setattr(d, "n_heads", 0), 2),
