@@ -15,9 +15,11 @@ import pytest
 
 import oracle.attention
 import oracle.decode
+import oracle.fidelity
 import oracle.layout
 import test_oracle_attention as TA
 import test_oracle_decode as TD
+import test_oracle_fidelity as TF
 import test_oracle_kmer_local as TK
 import test_oracle_layout as TL
 
@@ -68,6 +70,18 @@ def _kmer_local_pins():
         TK.test_first_kmer_is_textbook_causal(seed)
         TK.test_one_kmer_per_window_is_causal_plus_boundary(seed)
     TK.test_zero_kmer_single_window_is_dense_causal()
+
+
+def _fidelity_pins():
+    for V in (2, 4, 17):
+        TF.test_against_library_routines(V)
+        TF.test_point_mass_against_uniform(V)
+    TF.test_hellinger_forms_agree()
+    TF.test_identical_inputs_are_zero()
+    TF.test_point_masses_closed_forms()
+    TF.test_bounds_and_symmetry()
+    TF.test_softmax_and_clipping()
+    TF.test_sequence_means()
 
 
 def _decode_pins():
@@ -128,6 +142,19 @@ KMER_LOCAL_MUTATIONS = [
 ]
 
 
+FIDELITY_MUTATIONS = [
+    ("no renormalisation after the clip", "return p / p.sum(axis=-1, keepdims=True)", "return p"),
+    ("L2 without the root", "l2 = np.sqrt((d * d).sum(axis=-1))", "l2 = (d * d).sum(axis=-1)"),
+    ("Hellinger without 1/sqrt 2", " / np.sqrt(2.0)", ""),
+    ("JS against one side only", "js = 0.5 * kl(p, m) + 0.5 * kl(q, m)", "js = kl(p, m)"),
+    ("KL reversed", "kl(p, q)], axis=-1)", "kl(q, p)], axis=-1)"),
+    ("log base 2", "np.log(a / b)", "np.log2(a / b)"),
+    ("softmax over the wrong axis", "e / e.sum(axis=-1, keepdims=True)", "e / e.sum(axis=0, keepdims=True)"),
+    ("clip above instead of below", "np.maximum(np.asarray(p, np.float64), CLIP)",
+     "np.minimum(np.asarray(p, np.float64), 1 - CLIP)"),
+]
+
+
 def _expect_caught(monkeypatch, pins, patches):
     for mod_obj, attr, value in patches:
         monkeypatch.setattr(mod_obj, attr, value)
@@ -159,7 +186,14 @@ def test_kmer_local_mutations_are_caught(monkeypatch, name, old, new):
     _expect_caught(monkeypatch, _kmer_local_pins, [(TK, "A", mut)])
 
 
+@pytest.mark.parametrize("name,old,new", FIDELITY_MUTATIONS, ids=[m[0] for m in FIDELITY_MUTATIONS])
+def test_fidelity_mutations_are_caught(monkeypatch, name, old, new):
+    mut = _mutant(oracle.fidelity, old, new)
+    _expect_caught(monkeypatch, _fidelity_pins, [(TF, "FD", mut)])
+
+
 def test_unmutated_pins_pass():
+    _fidelity_pins()
     _layout_pins()
     _attention_pins()
     _decode_pins()
