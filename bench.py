@@ -18,7 +18,8 @@ Also reported on the same JSON line:
                 (whole windows, all heads), extrapolated by visible pairs
   secondary     compaction and decode (batch 16 at ~1 Mb) HBM rates, the dense
                 32 kb causal point, streaming (one window per call) prefill, and
-                the same 1 Mb prefill under the k-mer-local mask (HBM-bound)
+                the same 1 Mb prefill under the k-mer-local mask (HBM-bound), and
+                the fidelity metrics over 1 M positions (HBM-bound)
 """
 
 from __future__ import annotations
@@ -324,6 +325,29 @@ def secondary_kmer_local(torch, F, fw, s, timer, reps=5):
             "bound": "hbm", "frac_hbm": nbytes / (ms * 1e-3) / PEAK_HBM}
 
 
+def secondary_fidelity(torch, F, fw, reps=5):
+    """Fidelity metrics (L1, L2, Hellinger, JS, KL per position) over 1 M
+    positions, for 4 nucleotides (f32 logits) and a 512-entry vocabulary (bf16
+    logits).  Bound by HBM: both logit rows are read once, 5 floats written."""
+    res = {}
+    for name, (n, vocab, dtype) in fw.FIDELITY.items():
+        p, q = fw.fidelity_logits(n, vocab, dtype, seed=fw.BASE_SEED, device="cuda:0")
+        out = torch.empty(n, F.FOCUS_FID_N, dtype=torch.float32, device="cuda:0")
+        F.focus_fidelity(p, q, out=out)
+        e = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for a, b in e:
+            a.record()
+            F.focus_fidelity(p, q, out=out)
+            b.record()
+        torch.cuda.synchronize()
+        ms = sum(a.elapsed_time(b) for a, b in e) / reps
+        nbytes = 2 * n * vocab * p.element_size() + n * F.FOCUS_FID_N * 4
+        res[name] = {"positions": n, "vocab": vocab, "dtype": dtype, "ms": ms, "bytes": nbytes,
+                     "GBps": nbytes / ms / 1e6, "bound": "hbm", "frac_hbm": nbytes / (ms * 1e-3) / PEAK_HBM}
+        del p, q, out
+    return res
+
+
 def secondary_streaming(torch, F, s, n_windows=200):
     """Streaming prefill: one window per call (last n_windows windows)."""
     lay = s["lay"]
@@ -439,6 +463,9 @@ def main():
         torch.cuda.empty_cache()
         log("secondary: dense 32 kb")
         sec["dense_32kb"] = secondary_dense(torch, F, fw)
+        torch.cuda.empty_cache()
+        log("secondary: fidelity metrics")
+        sec["fidelity"] = secondary_fidelity(torch, F, fw)
         result["secondary"] = sec
     elif not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(torch, s, args.cpu_budget)

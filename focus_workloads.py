@@ -147,3 +147,25 @@ def qkv(n_rows: int, w: Workload, device="cpu", seed_offset: int = 0):
     k = randn((n_rows, w.kv_heads, w.head_dim), w.dtype, seed_for(w.index, "k") + seed_offset, device)
     v = randn((n_rows, w.kv_heads, w.head_dim), w.dtype, seed_for(w.index, "v") + seed_offset, device)
     return q, k, v
+
+
+# Next-base distributions for the fidelity metrics: the base model's logits are
+# N(0, scale^2) and the FOCUS model's are the same logits plus an independent
+# N(0, noise^2) perturbation (a compressed model close to its base).  Two
+# shapes: the four nucleotides, and a byte-level vocabulary of 512 entries.
+FIDELITY = {
+    # name: (positions, vocab, dtype)
+    "fidelity_1mb_acgt": (1_000_000, 4, "f32"),
+    "fidelity_1mb_vocab512": (1_000_000, 512, "bf16"),
+}
+
+
+def fidelity_logits(n_pos: int, vocab: int, dtype: str, seed: int, device="cpu",
+                    scale: float = 2.0, noise: float = 0.5):
+    """(p_logits, q_logits) [n_pos, vocab] as described above FIDELITY."""
+    base = randn((n_pos, vocab), "f32", seed, device) * scale
+    q = base + randn((n_pos, vocab), "f32", seed + 1, device) * noise
+    import torch
+    if dtype == "bf16":
+        return base.to(torch.bfloat16), q.to(torch.bfloat16)
+    return base, q

@@ -90,7 +90,7 @@ typedef void* focus_stream_t;   /* a hipStream_t */
 int32_t focus_abi_version(void);
 const char* focus_status_str(focus_status s);
 /* sizeof of the descriptor structs below, in declaration order
- * (0 totals, 1 layout, 2 compact, 3 attn, 4 decode); -1 otherwise.
+ * (0 totals, 1 layout, 2 compact, 3 attn, 4 decode, 5 fidelity); -1 otherwise.
  * Lets a binding check its mirror of the structs. */
 int64_t focus_struct_size(int32_t which);
 
@@ -335,6 +335,48 @@ size_t focus_decode_workspace(const focus_decode_desc* d);
  * An append into a full cache or window buffer is skipped with
  * FOCUS_ERR_CAPACITY (the step still attends over what is there). */
 focus_status focus_decode_step(const focus_decode_desc* d, focus_stream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Fidelity metrics                                                          */
+/* ------------------------------------------------------------------------ */
+
+/* Per-position distances between the base model's next-base distribution p_t
+ * and the FOCUS model's q_t over `vocab` categories (Appendix "Metrics"):
+ *   out[t, 0] = L1          sum_i |p_i - q_i|
+ *   out[t, 1] = L2          (sum_i (p_i - q_i)^2)^(1/2)
+ *   out[t, 2] = Hellinger   || sqrt p - sqrt q ||_2 / sqrt 2
+ *   out[t, 3] = JS          (KL(p || m) + KL(q || m)) / 2,  m = (p + q) / 2
+ *   out[t, 4] = KL          KL(p || q) = sum_i p_i ln(p_i / q_i)   (nats)
+ * Both distributions are clipped from below at 1e-12 and renormalised before
+ * every metric.  With FOCUS_FID_LOGITS the inputs are logits and the softmax
+ * is taken first; with FOCUS_FID_PROBS they are probabilities.  Arithmetic is
+ * float32.  If seq_mean is given, seq_mean[b, m] is the mean of out[t, m] over
+ * t in [cu_pos[b], cu_pos[b+1]) (0 for an empty sequence), the sequence-level
+ * score of the appendix; it needs out (unless n_pos is 0).
+ */
+enum { FOCUS_FID_LOGITS = 0, FOCUS_FID_PROBS = 1 };
+enum { FOCUS_FID_L1 = 0, FOCUS_FID_L2 = 1, FOCUS_FID_HELLINGER = 2, FOCUS_FID_JS = 3, FOCUS_FID_KL = 4,
+       FOCUS_FID_N = 5 };
+
+typedef struct {
+  int32_t dtype;                /* of p and q: FOCUS_BF16 or FOCUS_F32       */
+  int32_t input_kind;           /* FOCUS_FID_LOGITS or FOCUS_FID_PROBS       */
+  int64_t n_pos;                /* positions (rows of p and q)               */
+  int32_t vocab;                /* categories per row, 1 .. 1024             */
+  int32_t n_seq;                /* sequences of seq_mean (0: none)           */
+  const void* p;                /* [device][n_pos, vocab] row-major           */
+  const void* q;                /* [device][n_pos, vocab]                     */
+  float* out;                   /* [device][n_pos, FOCUS_FID_N]               */
+  const int64_t* cu_pos;        /* [device][n_seq + 1] row offsets, or NULL  */
+  float* seq_mean;              /* [device][n_seq, FOCUS_FID_N], or NULL      */
+  int32_t* err;                 /* optional error word                       */
+} focus_fidelity_desc;
+
+/* Errors: E_NULL, E_ARG (vocab, n_pos, input_kind, alignment: p and q aligned
+ * to their element size, out and seq_mean to 4 bytes; seq_mean without out or
+ * cu_pos), E_DTYPE, E_UNSUPPORTED (vocab > 1024), E_HIP.  Sequences whose
+ * offsets fall outside [0, n_pos] get FOCUS_ERR_BOUNDS and a zero mean. */
+focus_status focus_fidelity(const focus_fidelity_desc* d, focus_stream_t stream);
 
 #ifdef __cplusplus
 }

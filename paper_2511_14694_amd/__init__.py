@@ -23,14 +23,16 @@ from typing import Dict, Optional
 import numpy as np
 import torch
 
-from ._abi import (AttnDesc, CompactDesc, DecodeDesc, FocusError, LayoutDesc, LayoutTotals,
+from ._abi import (AttnDesc, CompactDesc, DecodeDesc, FidelityDesc, FocusError, LayoutDesc, LayoutTotals,
                    FOCUS_BF16, FOCUS_F32, FOCUS_MASK_CT, FOCUS_MASK_KMER_LOCAL,
                    FOCUS_TOK_BASE, FOCUS_TOK_SUMMARY, FOCUS_STEP_SUMMARY, FOCUS_STEP_WINDOW_END,
-                   FOCUS_ERR_CAPACITY, FOCUS_ERR_BOUNDS, FOCUS_ERR_PLAN, check, lib)
+                   FOCUS_ERR_CAPACITY, FOCUS_ERR_BOUNDS, FOCUS_ERR_PLAN,
+                   FOCUS_FID_LOGITS, FOCUS_FID_PROBS, FOCUS_FID_N, check, lib)
 
 __all__ = ["focus_layout_plan", "focus_layout", "focus_compact_kv", "focus_window_attn",
            "focus_window_attn_workspace", "focus_decode_step", "focus_decode_workspace",
-           "focus_abi_version", "Layout", "LayoutTotals", "FocusError",
+           "focus_fidelity", "focus_abi_version", "Layout", "LayoutTotals", "FocusError",
+           "FOCUS_FID_LOGITS", "FOCUS_FID_PROBS", "FOCUS_FID_N",
            "FOCUS_BF16", "FOCUS_F32", "FOCUS_MASK_CT", "FOCUS_MASK_KMER_LOCAL",
            "FOCUS_TOK_BASE", "FOCUS_TOK_SUMMARY", "FOCUS_STEP_SUMMARY", "FOCUS_STEP_WINDOW_END",
            "FOCUS_ERR_CAPACITY", "FOCUS_ERR_BOUNDS", "FOCUS_ERR_PLAN"]
@@ -270,3 +272,32 @@ def focus_decode_step(q, k_new, v_new, kind, cache_k, cache_v, cache_len, win_k,
                      o, lse, workspace, split_keys, softmax_scale, err)
     check("focus_decode_step", lib().focus_decode_step(C.byref(d), _stream(stream, q.device)))
     return o, lse
+
+
+def focus_fidelity(p, q, input_kind: int = FOCUS_FID_LOGITS, cu_pos=None, out=None, seq_mean=None,
+                   err=None, stream=None):
+    """Per-position L1 / L2 / Hellinger / JS / KL between the rows of p and q
+    ([n_pos, vocab], logits or probabilities); with cu_pos ([n_seq + 1] row
+    offsets) also the per-sequence means.  Returns (out [n_pos, 5], seq_mean)."""
+    if p.shape != q.shape or p.dtype != q.dtype or p.dim() != 2 or not p.is_contiguous() \
+            or not q.is_contiguous():
+        raise ValueError("p and q must be contiguous [n_pos, vocab] tensors of one dtype")
+    n_pos, vocab = p.shape
+    if out is None:
+        out = torch.empty(n_pos, FOCUS_FID_N, dtype=torch.float32, device=p.device)
+    if tuple(out.shape) != (n_pos, FOCUS_FID_N) or out.dtype != torch.float32:
+        raise ValueError("out must be float32 [n_pos, 5]")
+    n_seq = 0
+    if cu_pos is not None:
+        cu_pos = torch.as_tensor(cu_pos, dtype=torch.int64).to(p.device).contiguous()
+        n_seq = cu_pos.numel() - 1
+        if seq_mean is None:
+            seq_mean = torch.empty(n_seq, FOCUS_FID_N, dtype=torch.float32, device=p.device)
+    d = FidelityDesc()
+    d.dtype = _dtype(p)
+    d.input_kind = int(input_kind)
+    d.n_pos, d.vocab, d.n_seq = n_pos, vocab, n_seq
+    d.p, d.q, d.out = _ptr(p), _ptr(q), _ptr(out)
+    d.cu_pos, d.seq_mean, d.err = _ptr(cu_pos), _ptr(seq_mean), _ptr(err)
+    check("focus_fidelity", lib().focus_fidelity(C.byref(d), _stream(stream, p.device)))
+    return out, seq_mean

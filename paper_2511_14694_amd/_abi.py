@@ -16,6 +16,8 @@ FOCUS_MASK_CT, FOCUS_MASK_KMER_LOCAL = 0, 1
 FOCUS_TOK_BASE, FOCUS_TOK_SUMMARY = 0, 1
 FOCUS_STEP_SUMMARY, FOCUS_STEP_WINDOW_END = 1, 2
 FOCUS_ERR_CAPACITY, FOCUS_ERR_BOUNDS, FOCUS_ERR_PLAN = 1, 2, 4
+FOCUS_FID_LOGITS, FOCUS_FID_PROBS = 0, 1
+FOCUS_FID_N = 5
 
 p = C.c_void_p
 i32, i64, f32, sz = C.c_int32, C.c_int64, C.c_float, C.c_size_t
@@ -69,7 +71,12 @@ class DecodeDesc(C.Structure):
                 ("o", p), ("lse", p), ("workspace", p), ("workspace_bytes", sz), ("err", p)]
 
 
-STRUCTS = [LayoutTotals, LayoutDesc, CompactDesc, AttnDesc, DecodeDesc]
+class FidelityDesc(C.Structure):
+    _fields_ = [("dtype", i32), ("input_kind", i32), ("n_pos", i64), ("vocab", i32), ("n_seq", i32),
+                ("p", p), ("q", p), ("out", p), ("cu_pos", p), ("seq_mean", p), ("err", p)]
+
+
+STRUCTS = [LayoutTotals, LayoutDesc, CompactDesc, AttnDesc, DecodeDesc, FidelityDesc]
 
 # name -> (restype, argtypes): every symbol include/focus.h declares
 SYMBOLS = {
@@ -83,6 +90,7 @@ SYMBOLS = {
     "focus_window_attn": (i32, [C.POINTER(AttnDesc), p]),
     "focus_decode_workspace": (sz, [C.POINTER(DecodeDesc)]),
     "focus_decode_step": (i32, [C.POINTER(DecodeDesc), p]),
+    "focus_fidelity": (i32, [C.POINTER(FidelityDesc), p]),
 }
 
 

@@ -26,6 +26,7 @@ extern "C" int64_t focus_struct_size(int32_t which) {
     case 2: return sizeof(focus_compact_desc);
     case 3: return sizeof(focus_attn_desc);
     case 4: return sizeof(focus_decode_desc);
+    case 5: return sizeof(focus_fidelity_desc);
     default: return -1;
   }
 }

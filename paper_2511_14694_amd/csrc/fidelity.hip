@@ -1,0 +1,333 @@
+// Fidelity metrics between two next-base distributions (focus_fidelity):
+// L1, L2, Hellinger, Jensen-Shannon and KL(p || q) of the Metrics appendix,
+// after clipping both distributions at 1e-12 and renormalising, per position;
+// optionally the per-sequence mean of each metric.
+//
+// Bound by HBM: every input element is read once.  Rows of up to 8 categories
+// (the four nucleotides) take one thread per position with the whole row in
+// registers; longer rows (a byte-level vocabulary) take one wave per position,
+// each lane holding up to 16 of the row's elements, with wave reductions.
+// Logarithms are base 2 (v_log_f32) scaled by ln 2 once per sum.
+#include "common.h"
+
+#include <math.h>
+
+namespace {
+
+constexpr float kClip = 1e-12f;
+constexpr float kLog2e = 1.44269504088896341f;
+constexpr float kLn2 = 0.69314718055994531f;
+constexpr int kSmallV = 8;       // rows up to this long: one thread per position
+constexpr int kMaxPerLane = 16;  // wave path: elements per lane, vocab <= 1024
+constexpr int kThreads = 256;
+
+template <typename T> __device__ inline float ld(const T* p, int64_t i);
+template <> __device__ inline float ld<float>(const float* p, int64_t i) { return p[i]; }
+template <> __device__ inline float ld<__bf16>(const __bf16* p, int64_t i) { return (float)p[i]; }
+
+// Wave-wide sum / max, the result in every lane: DPP inside rows of 16 lanes
+// (quad swaps, then the half-row and row mirrors), one swizzle across the two
+// rows of each half-wave, and v_permlane32_swap across the halves.
+__device__ inline float dpp_mirror16(float x) {  // lane i <-> lane 15-i within 16
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x140, 0xF, 0xF, false));
+}
+__device__ inline float wave_sum(float x) {
+  x = focus::sum8(x);
+  x += dpp_mirror16(x);
+  x += __shfl_xor(x, 16);
+  const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+}
+__device__ inline float wave_max(float x) {
+  x = fmaxf(x, focus::dpp_xor1(x));
+  x = fmaxf(x, focus::dpp_xor2(x));
+  x = fmaxf(x, focus::dpp_half_mirror(x));
+  x = fmaxf(x, dpp_mirror16(x));
+  x = fmaxf(x, __shfl_xor(x, 16));
+  const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+}
+
+// Accumulates the metric sums of one pair of clipped, renormalised
+// probabilities: |d|, d^2, (sqrt p - sqrt q)^2, the JS terms and the KL term
+// (the last two in log2 units).
+struct Sums {
+  float l1 = 0.f, l2 = 0.f, h = 0.f, js = 0.f, kl = 0.f;
+  __device__ void add(float p, float q) {
+    const float d = p - q;
+    l1 += fabsf(d);
+    l2 = fmaf(d, d, l2);
+    const float s = sqrtf(p) - sqrtf(q);
+    h = fmaf(s, s, h);
+    const float lp = __builtin_amdgcn_logf(p), lq = __builtin_amdgcn_logf(q);
+    const float lm = __builtin_amdgcn_logf(0.5f * (p + q));
+    js += p * (lp - lm) + q * (lq - lm);
+    kl = fmaf(p, lp - lq, kl);
+  }
+  __device__ void store(float* out) const {
+    out[FOCUS_FID_L1] = l1;
+    out[FOCUS_FID_L2] = sqrtf(l2);
+    out[FOCUS_FID_HELLINGER] = sqrtf(0.5f * h);
+    out[FOCUS_FID_JS] = 0.5f * kLn2 * js;
+    out[FOCUS_FID_KL] = kLn2 * kl;
+  }
+};
+
+// One thread per position, vocab <= kSmallV.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void fid_rows_small(focus_fidelity_desc d) {
+  const int64_t t = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (t >= d.n_pos) return;
+  const int V = d.vocab;
+  const T* pr = reinterpret_cast<const T*>(d.p) + t * V;
+  const T* qr = reinterpret_cast<const T*>(d.q) + t * V;
+  float p[kSmallV], q[kSmallV];
+  float mp = -INFINITY, mq = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < kSmallV; ++i) {
+    p[i] = i < V ? ld(pr, i) : 0.f;
+    q[i] = i < V ? ld(qr, i) : 0.f;
+    if (i < V) {
+      mp = fmaxf(mp, p[i]);
+      mq = fmaxf(mq, q[i]);
+    }
+  }
+  float sp = 0.f, sq = 0.f;
+#pragma unroll
+  for (int i = 0; i < kSmallV; ++i) {
+    if (i < V) {
+      if (d.input_kind == FOCUS_FID_LOGITS) {
+        p[i] = __builtin_amdgcn_exp2f((p[i] - mp) * kLog2e);
+        q[i] = __builtin_amdgcn_exp2f((q[i] - mq) * kLog2e);
+      }
+      sp += p[i];
+      sq += q[i];
+    }
+  }
+  // finish the softmax (logits only), clip, renormalise
+  if (d.input_kind != FOCUS_FID_LOGITS) sp = sq = 1.f;
+  float cp = 0.f, cq = 0.f;
+#pragma unroll
+  for (int i = 0; i < kSmallV; ++i) {
+    if (i < V) {
+      p[i] = fmaxf(p[i] / sp, kClip);
+      q[i] = fmaxf(q[i] / sq, kClip);
+      cp += p[i];
+      cq += q[i];
+    }
+  }
+  Sums m;
+#pragma unroll
+  for (int i = 0; i < kSmallV; ++i)
+    if (i < V) m.add(p[i] / cp, q[i] / cq);
+  m.store(d.out + t * FOCUS_FID_N);
+}
+
+// One wave per position, kSmallV < vocab <= 64 * NPL (NPL = 8 or 16).  VEC: the row is
+// read 16 bytes per lane per load (kVec elements), else one element per load.
+// Logarithms of the clipped, renormalised probabilities come straight from the
+// logits (log2 p = (x - max) log2 e - log2 sum, or log2 of the clip); the
+// mixture's logarithm is built from them, and no division is left per element.
+template <typename T, bool VEC, int NPL, bool FULL>
+__global__ __launch_bounds__(kThreads) void fid_rows_wave(focus_fidelity_desc d) {
+  constexpr int kVec = 16 / sizeof(T);
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+  if (t >= d.n_pos) return;
+  const int V = d.vocab;
+  const bool logits = d.input_kind == FOCUS_FID_LOGITS;
+  const T* pr = reinterpret_cast<const T*>(d.p) + t * V;
+  const T* qr = reinterpret_cast<const T*>(d.q) + t * V;
+  auto elem = [&](int k) { return VEC ? (k / kVec) * 64 * kVec + lane * kVec + k % kVec : lane + 64 * k; };
+  // FULL: vocab == 64 NPL, every element of every lane is in the row
+  bool ok[NPL];
+#pragma unroll
+  for (int k = 0; k < NPL; ++k) ok[k] = FULL || elem(k) < V;
+  float xp[NPL], xq[NPL];
+  if constexpr (VEC) {
+#pragma unroll
+    for (int c = 0; c < NPL / kVec; ++c) {
+      const int i0 = c * 64 * kVec + lane * kVec;
+      uint4 wp = make_uint4(0, 0, 0, 0), wq = wp;
+      if (i0 < V) {
+        wp = *reinterpret_cast<const uint4*>(pr + i0);
+        wq = *reinterpret_cast<const uint4*>(qr + i0);
+      }
+      const T* ep = reinterpret_cast<const T*>(&wp);
+      const T* eq = reinterpret_cast<const T*>(&wq);
+#pragma unroll
+      for (int j = 0; j < kVec; ++j) {
+        xp[c * kVec + j] = (float)ep[j];
+        xq[c * kVec + j] = (float)eq[j];
+      }
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < NPL; ++k) {
+      const int i = elem(k);
+      xp[k] = i < V ? ld(pr, i) : 0.f;
+      xq[k] = i < V ? ld(qr, i) : 0.f;
+    }
+  }
+  float mp = -INFINITY, mq = -INFINITY;
+  if (logits) {
+#pragma unroll
+    for (int k = 0; k < NPL; ++k)
+      if (ok[k]) {
+        mp = fmaxf(mp, xp[k]);
+        mq = fmaxf(mq, xq[k]);
+      }
+    mp = wave_max(mp);
+    mq = wave_max(mq);
+  }
+  // p = softmax(x) (logits) or x (probabilities); then the clip
+  float p[NPL], q[NPL];
+  float sp = 0.f, sq = 0.f;
+#pragma unroll
+  for (int k = 0; k < NPL; ++k) {
+    p[k] = logits ? __builtin_amdgcn_exp2f((xp[k] - mp) * kLog2e) : xp[k];
+    q[k] = logits ? __builtin_amdgcn_exp2f((xq[k] - mq) * kLog2e) : xq[k];
+    if (ok[k]) {
+      sp += p[k];
+      sq += q[k];
+    }
+  }
+  float rp = 1.f, rq = 1.f, lsp = 0.f, lsq = 0.f;
+  if (logits) {
+    sp = wave_sum(sp);
+    sq = wave_sum(sq);
+    rp = 1.f / sp;
+    rq = 1.f / sq;
+    lsp = __builtin_amdgcn_logf(sp);
+    lsq = __builtin_amdgcn_logf(sq);
+  }
+  float cp = 0.f, cq = 0.f;
+#pragma unroll
+  for (int k = 0; k < NPL; ++k) {
+    p[k] = fmaxf(p[k] * rp, kClip);
+    q[k] = fmaxf(q[k] * rq, kClip);
+    if (ok[k]) {
+      cp += p[k];
+      cq += q[k];
+    }
+  }
+  cp = wave_sum(cp);
+  cq = wave_sum(cq);
+  const float rcp = 1.f / cp, rcq = 1.f / cq;
+  const float lcp = __builtin_amdgcn_logf(cp), lcq = __builtin_amdgcn_logf(cq);
+  const float lclip = __builtin_amdgcn_logf(kClip);
+  float l1 = 0.f, l2 = 0.f, h = 0.f, js = 0.f, kl = 0.f;
+#pragma unroll
+  for (int k = 0; k < NPL; ++k) {
+    if (!ok[k]) continue;
+    const float pn = p[k] * rcp, qn = q[k] * rcq;
+    float lp, lq;
+    if (logits) {
+      lp = (p[k] > kClip ? (xp[k] - mp) * kLog2e - lsp : lclip) - lcp;
+      lq = (q[k] > kClip ? (xq[k] - mq) * kLog2e - lsq : lclip) - lcq;
+    } else {
+      lp = __builtin_amdgcn_logf(pn);
+      lq = __builtin_amdgcn_logf(qn);
+    }
+    const float dd = pn - qn;
+    l1 += fabsf(dd);
+    l2 = fmaf(dd, dd, l2);
+    const float sd = sqrtf(pn) - sqrtf(qn);
+    h = fmaf(sd, sd, h);
+    // log2 m from lp and lq (exactly lp when lp == lq, so identical inputs
+    // give an exact zero): m = 2^max * (1 + 2^-|lp - lq|) / 2
+    const float lm = fmaxf(lp, lq) + __builtin_amdgcn_logf(0.5f + 0.5f * __builtin_amdgcn_exp2f(-fabsf(lp - lq)));
+    js += pn * (lp - lm) + qn * (lq - lm);
+    kl = fmaf(pn, lp - lq, kl);
+  }
+  Sums m;
+  m.l1 = wave_sum(l1);
+  m.l2 = wave_sum(l2);
+  m.h = wave_sum(h);
+  m.js = wave_sum(js);
+  m.kl = wave_sum(kl);
+  if (lane == 0) m.store(d.out + t * FOCUS_FID_N);
+}
+
+// Mean of each metric over a sequence's positions: one workgroup per
+// sequence, a fixed-order tree sum (deterministic).
+__global__ __launch_bounds__(kThreads) void fid_seq_mean(focus_fidelity_desc d) {
+  const int b = blockIdx.x;
+  __shared__ float red[FOCUS_FID_N][kThreads];
+  const int64_t t0 = d.cu_pos[b], t1 = d.cu_pos[b + 1];
+  const bool ok = t0 >= 0 && t1 >= t0 && t1 <= d.n_pos;
+  if (!ok && threadIdx.x == 0) focus::raise_err(d.err, FOCUS_ERR_BOUNDS);
+  float acc[FOCUS_FID_N] = {0.f, 0.f, 0.f, 0.f, 0.f};
+  if (ok)
+    for (int64_t t = t0 + threadIdx.x; t < t1; t += kThreads)
+#pragma unroll
+      for (int m = 0; m < FOCUS_FID_N; ++m) acc[m] += d.out[t * FOCUS_FID_N + m];
+#pragma unroll
+  for (int m = 0; m < FOCUS_FID_N; ++m) red[m][threadIdx.x] = acc[m];
+  __syncthreads();
+  for (int s = kThreads / 2; s > 0; s >>= 1) {
+    if ((int)threadIdx.x < s)
+#pragma unroll
+      for (int m = 0; m < FOCUS_FID_N; ++m) red[m][threadIdx.x] += red[m][threadIdx.x + s];
+    __syncthreads();
+  }
+  if ((int)threadIdx.x < FOCUS_FID_N) {
+    const int64_t n = ok ? t1 - t0 : 0;
+    d.seq_mean[(int64_t)b * FOCUS_FID_N + threadIdx.x] = n > 0 ? red[threadIdx.x][0] / (float)n : 0.f;
+  }
+}
+
+}  // namespace
+
+extern "C" focus_status focus_fidelity(const focus_fidelity_desc* d, focus_stream_t stream) {
+  if (!d) return FOCUS_E_NULL;
+  if (d->dtype != FOCUS_BF16 && d->dtype != FOCUS_F32) return FOCUS_E_DTYPE;
+  if (d->input_kind != FOCUS_FID_LOGITS && d->input_kind != FOCUS_FID_PROBS) return FOCUS_E_ARG;
+  if (d->n_pos < 0 || d->vocab < 1 || d->n_seq < 0) return FOCUS_E_ARG;
+  if (d->vocab > 64 * kMaxPerLane) return FOCUS_E_UNSUPPORTED;
+  const bool want_mean = d->n_seq > 0 && d->seq_mean;
+  if (want_mean && (!d->cu_pos || (d->n_pos > 0 && !d->out))) return FOCUS_E_ARG;
+  if (d->n_pos > 0 && (!d->p || !d->q || !d->out)) return FOCUS_E_NULL;
+  const uintptr_t ea = (uintptr_t)focus::elt_bytes(d->dtype) - 1;
+  if ((reinterpret_cast<uintptr_t>(d->p) & ea) || (reinterpret_cast<uintptr_t>(d->q) & ea) ||
+      (reinterpret_cast<uintptr_t>(d->out) & 3u) || (reinterpret_cast<uintptr_t>(d->seq_mean) & 3u) ||
+      (reinterpret_cast<uintptr_t>(d->cu_pos) & 7u))
+    return FOCUS_E_ARG;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (d->n_pos > 0) {
+    const bool small = d->vocab <= kSmallV;
+    const int64_t per_block = small ? kThreads : kThreads / 64;
+    const int64_t blocks = focus::ceil_div(d->n_pos, per_block);
+    if (blocks > INT32_MAX) return FOCUS_E_SHAPE;
+    const dim3 grid((uint32_t)blocks), block(kThreads);
+    // 16-byte row loads when every row starts 16-byte aligned
+    const int64_t eb = focus::elt_bytes(d->dtype);
+    const bool vec = (d->vocab * eb) % 16 == 0 && focus::aligned16(d->p) && focus::aligned16(d->q);
+    const bool wide = d->vocab > 512;
+#define FOCUS_FID_WAVE(T)                                                                        \
+  if (wide) {                                                                                    \
+    if (vec && d->vocab == 1024) hipLaunchKernelGGL((fid_rows_wave<T, true, 16, true>), grid, block, 0, s, *d);   \
+    else if (vec) hipLaunchKernelGGL((fid_rows_wave<T, true, 16, false>), grid, block, 0, s, *d);  \
+    else hipLaunchKernelGGL((fid_rows_wave<T, false, 16, false>), grid, block, 0, s, *d);          \
+  } else {                                                                                       \
+    if (vec && d->vocab == 512) hipLaunchKernelGGL((fid_rows_wave<T, true, 8, true>), grid, block, 0, s, *d);     \
+    else if (vec) hipLaunchKernelGGL((fid_rows_wave<T, true, 8, false>), grid, block, 0, s, *d);   \
+    else hipLaunchKernelGGL((fid_rows_wave<T, false, 8, false>), grid, block, 0, s, *d);           \
+  }
+    if (d->dtype == FOCUS_BF16) {
+      if (small) hipLaunchKernelGGL(fid_rows_small<__bf16>, grid, block, 0, s, *d);
+      else { FOCUS_FID_WAVE(__bf16) }
+    } else {
+      if (small) hipLaunchKernelGGL(fid_rows_small<float>, grid, block, 0, s, *d);
+      else { FOCUS_FID_WAVE(float) }
+    }
+#undef FOCUS_FID_WAVE
+    focus_status st = focus::launch_status();
+    if (st != FOCUS_OK) return st;
+  }
+  if (want_mean) {
+    hipLaunchKernelGGL(fid_seq_mean, dim3(d->n_seq), dim3(kThreads), 0, s, *d);
+    return focus::launch_status();
+  }
+  return FOCUS_OK;
+}

@@ -205,3 +205,27 @@ def test_layout_host_validation(mutate, status):
         setattr(d, f, fake)
     mutate(d)
     assert _call("focus_layout", d) == status
+
+
+def _fid_ok():
+    d = _abi.FidelityDesc()
+    d.dtype, d.input_kind, d.n_pos, d.vocab = 1, 0, 10, 4
+    fake = 1 << 20
+    d.p, d.q, d.out = fake, fake, fake
+    return d
+
+
+@pytest.mark.parametrize("mutate,status", [
+    (lambda d: setattr(d, "dtype", 9), 4),
+    (lambda d: setattr(d, "input_kind", 3), 2),
+    (lambda d: setattr(d, "vocab", 0), 2),
+    (lambda d: setattr(d, "vocab", 1025), 5),
+    (lambda d: setattr(d, "n_pos", -1), 2),
+    (lambda d: setattr(d, "p", None), 1),
+    (lambda d: setattr(d, "q", (1 << 20) + 2), 2),
+    (lambda d: (setattr(d, "n_seq", 2), setattr(d, "seq_mean", 1 << 20)), 2),   # no cu_pos
+])
+def test_fidelity_host_validation(mutate, status):
+    d = _fid_ok()
+    mutate(d)
+    assert _call("focus_fidelity", d) == status
