@@ -13,10 +13,12 @@ import sys
 
 import pytest
 
+import oracle.adapter
 import oracle.attention
 import oracle.decode
 import oracle.fidelity
 import oracle.layout
+import test_oracle_adapter as TAD
 import test_oracle_attention as TA
 import test_oracle_decode as TD
 import test_oracle_fidelity as TF
@@ -82,6 +84,18 @@ def _fidelity_pins():
     TF.test_bounds_and_symmetry()
     TF.test_softmax_and_clipping()
     TF.test_sequence_means()
+
+
+def _adapter_pins():
+    for seed in range(3):
+        for mask in ("ct", "kmer_local"):
+            TAD.test_summary_rows_of_the_main_attention(mask, seed)
+        TAD.test_zero_keys_one_hot_values_count_the_visible_set(seed)
+    TAD.test_identity_projections_give_the_attention()
+    TAD.test_linear_in_output_and_value_weights()
+    TAD.test_grouped_kv_heads_equal_repeated_heads()
+    for mask in ("ct", "kmer_local"):
+        TAD.test_causality_and_windows_without_summaries(mask)
 
 
 def _decode_pins():
@@ -155,6 +169,16 @@ FIDELITY_MUTATIONS = [
 ]
 
 
+ADAPTER_MUTATIONS = [
+    ("summary rows shifted", 'rows = layout["sum_tok"][s0:s0 + B] - t0', 'rows = layout["sum_tok"][s0:s0 + B] - t0 - 1'),
+    ("no output projection", "return o.reshape(len(q_sum), n_heads * D) @ w_o",
+     "return o.reshape(len(q_sum), n_heads * D)"),
+    ("queries of the wrong tokens", 'hidden[layout["sum_tok"]] @ w_q', 'hidden[layout["sum_tok"] - 1] @ w_q'),
+    ("k-mer-local rule ignored", 'if mask == "kmer_local":\n        return A.kmer_local_window_visibility(layout, w)',
+     'if mask == "kmer_local":\n        return A.window_visibility(int(layout["win_ntok"][w]), int(layout["win_cache_off"][w]))'),
+]
+
+
 def _expect_caught(monkeypatch, pins, patches):
     for mod_obj, attr, value in patches:
         monkeypatch.setattr(mod_obj, attr, value)
@@ -192,7 +216,14 @@ def test_fidelity_mutations_are_caught(monkeypatch, name, old, new):
     _expect_caught(monkeypatch, _fidelity_pins, [(TF, "FD", mut)])
 
 
+@pytest.mark.parametrize("name,old,new", ADAPTER_MUTATIONS, ids=[m[0] for m in ADAPTER_MUTATIONS])
+def test_adapter_mutations_are_caught(monkeypatch, name, old, new):
+    mut = _mutant(oracle.adapter, old, new)
+    _expect_caught(monkeypatch, _adapter_pins, [(TAD, "AD", mut)])
+
+
 def test_unmutated_pins_pass():
+    _adapter_pins()
     _fidelity_pins()
     _layout_pins()
     _attention_pins()
