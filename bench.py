@@ -18,8 +18,9 @@ Also reported on the same JSON line:
                 (whole windows, all heads), extrapolated by visible pairs
   secondary     compaction and decode (batch 16 at ~1 Mb) HBM rates, the dense
                 32 kb causal point, streaming (one window per call) prefill, and
-                the same 1 Mb prefill under the k-mer-local mask (HBM-bound), and
-                the fidelity metrics over 1 M positions (HBM-bound)
+                the same 1 Mb prefill under the k-mer-local mask (HBM-bound), the
+                fidelity metrics over 1 M positions (HBM-bound), and the FOCUS
+                adapter update of the summary tokens at 1 Mb (d_model 4096)
 """
 
 from __future__ import annotations
@@ -348,6 +349,68 @@ def secondary_fidelity(torch, F, fw, reps=5):
     return res
 
 
+def secondary_adapter(torch, F, fw, reps=3, d_model=4096):
+    """The FOCUS adapter update of the summary tokens (eq. focus-attn) on the
+    1 Mb layout with an Evo-2-scale layer (d_model 4096, 32 x 128): W_K / W_V
+    over every token, the adapter's retained K/V, W_Q over the summaries, the
+    summary-query attention and W_O.  Random weights N(0, 1/d)."""
+    w = fw.WORKLOADS["prefill_1mb"]
+    H, Hkv, D = w.heads, w.kv_heads, w.head_dim
+    seq = [w.seq_nt] * w.batch
+    km = fw.kmer_draw(w)
+    tot = F.focus_layout_plan(seq, w.window_nt, km)
+    lay = F.focus_layout(tot, seq, w.window_nt, km, device="cuda:0")
+    hid = fw.randn((tot.n_tokens, d_model), "bf16", fw.BASE_SEED, "cuda:0")
+    sc = 1.0 / np.sqrt(d_model)
+    wq = (fw.randn((d_model, H * D), "f32", 1, "cuda:0") * sc).to(torch.bfloat16)
+    wk = (fw.randn((d_model, Hkv * D), "f32", 2, "cuda:0") * sc).to(torch.bfloat16)
+    wv = (fw.randn((d_model, Hkv * D), "f32", 3, "cuda:0") * sc).to(torch.bfloat16)
+    wo = (fw.randn((H * D, d_model), "f32", 4, "cuda:0") / np.sqrt(H * D)).to(torch.bfloat16)
+    ws = torch.empty(F.focus_adapter_layer_workspace(lay, hid, wq, wk, wv, wo, H, Hkv), dtype=torch.uint8,
+                     device="cuda:0")
+    out = torch.empty(tot.n_summaries, d_model, dtype=torch.bfloat16, device="cuda:0")
+    F.focus_adapter_layer(lay, hid, wq, wk, wv, wo, H, Hkv, out=out, workspace=ws)
+    e = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for a, b in e:
+        a.record()
+        F.focus_adapter_layer(lay, hid, wq, wk, wv, wo, H, Hkv, out=out, workspace=ws)
+        b.record()
+    torch.cuda.synchronize()
+    ms = sum(a.elapsed_time(b) for a, b in e) / reps
+    # the attention alone, on the workspace's projections (same launch the layer makes)
+    nt, ns = tot.n_tokens, tot.n_summaries
+    kv_b = nt * Hkv * D * 2
+    k = ws[:kv_b].view(torch.bfloat16).view(nt, Hkv, D)
+    off = -(-kv_b // 256) * 256
+    v = ws[off:off + kv_b].view(torch.bfloat16).view(nt, Hkv, D)
+    qs = torch.empty(ns, H, D, dtype=torch.bfloat16, device="cuda:0")
+    F.focus_gemm(hid, wq, out=qs.view(ns, H * D), a_rows=lay["sum_tok"])
+    cap = max(tot.max_cache_per_seq, 1)
+    ck = torch.empty(w.batch, cap, Hkv, D, dtype=torch.bfloat16, device="cuda:0")
+    cv = torch.empty_like(ck)
+    F.focus_compact_kv(lay, k, v, ck, cv)
+    F.focus_adapter_attn(lay, qs, k, v, ck, cv)
+    a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a0.record()
+    for _ in range(reps):
+        F.focus_adapter_attn(lay, qs, k, v, ck, cv)
+    a1.record()
+    torch.cuda.synchronize()
+    attn_ms = a0.elapsed_time(a1) / reps
+    st = lay["sum_tok"].cpu().numpy()
+    win_of = np.repeat(np.arange(tot.n_windows), lay["win_nsum"].cpu().numpy())
+    rows = st - lay["win_tok_off"].cpu().numpy()[win_of]
+    pairs = int((lay["win_cache_off"].cpu().numpy()[win_of].astype(np.int64) + rows + 1).sum())
+    attn_flops = 4 * D * H * pairs
+    gemm_flops = 2 * nt * d_model * 2 * Hkv * D + 2 * ns * d_model * H * D * 2
+    flops = attn_flops + gemm_flops
+    return {"workload": f"prefill_1mb layout, d_model {d_model}, {H} x {D} heads, bf16, random weights",
+            "ms": ms, "tflops": flops / ms / 1e9, "frac_mfma": flops / (ms * 1e-3) / PEAK_BF16_FLOPS,
+            "gemm_flops": gemm_flops, "attention": {"ms": attn_ms, "visible_pairs_per_head": pairs,
+                                                    "tflops": attn_flops / attn_ms / 1e9,
+                                                    "frac_mfma": attn_flops / (attn_ms * 1e-3) / PEAK_BF16_FLOPS}}
+
+
 def secondary_streaming(torch, F, s, n_windows=200):
     """Streaming prefill: one window per call (last n_windows windows)."""
     lay = s["lay"]
@@ -466,6 +529,9 @@ def main():
         torch.cuda.empty_cache()
         log("secondary: fidelity metrics")
         sec["fidelity"] = secondary_fidelity(torch, F, fw)
+        torch.cuda.empty_cache()
+        log("secondary: FOCUS adapter layer")
+        sec["adapter_1mb"] = secondary_adapter(torch, F, fw)
         result["secondary"] = sec
     elif not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(torch, s, args.cpu_budget)

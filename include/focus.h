@@ -90,7 +90,8 @@ typedef void* focus_stream_t;   /* a hipStream_t */
 int32_t focus_abi_version(void);
 const char* focus_status_str(focus_status s);
 /* sizeof of the descriptor structs below, in declaration order
- * (0 totals, 1 layout, 2 compact, 3 attn, 4 decode, 5 fidelity); -1 otherwise.
+ * (0 totals, 1 layout, 2 compact, 3 attn, 4 decode, 5 fidelity, 6 gemm,
+ * 7 adapter, 8 adapter layer); -1 otherwise.
  * Lets a binding check its mirror of the structs. */
 int64_t focus_struct_size(int32_t which);
 
@@ -377,6 +378,142 @@ typedef struct {
  * cu_pos), E_DTYPE, E_UNSUPPORTED (vocab > 1024), E_HIP.  Sequences whose
  * offsets fall outside [0, n_pos] get FOCUS_ERR_BOUNDS and a zero mean. */
 focus_status focus_fidelity(const focus_fidelity_desc* d, focus_stream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* FOCUS adapter attention                                                   */
+/* ------------------------------------------------------------------------ */
+
+/* The summary tokens' attention of the FOCUS adapter (Appendix A eq.
+ * focus-attn): for every listed window w of sequence b, every head h and every
+ * summary s of w (global summary index, token t = sum_tok[s], window row
+ * i = t - win_tok_off[w]):
+ *     keys     = [cache_k[b, 0:C_w, g] ; k[window rows, g]],  g = h / (H / H_kv)
+ *     visible  = as focus_window_attn's row i under `mask` (C(t): the paper's
+ *                visible set of the adapter; k-mer-local: Sec. 3.2's own k-mer
+ *                plus earlier summaries of the window plus the carried boundary)
+ *     o_sum[s - sum_base, h]   = softmax(scale * q_sum[s - sum_base, h] . keys^T) . values
+ *     lse_sum[s - sum_base, h] = log sum_visible exp(...)
+ * k / v hold the adapter's key / value projections of the window tokens (row
+ * r = token kv_tok_base + r); cache_k / cache_v those of the earlier windows'
+ * summaries, as focus_compact_kv leaves them.  Only the summary queries are
+ * computed (B_w per window instead of T_w).  bf16 only.
+ * Errors: as focus_window_attn; E_UNSUPPORTED for f32.  A window whose rows or
+ * summaries fall outside the buffers is skipped with FOCUS_ERR_BOUNDS. */
+typedef struct {
+  focus_layout_totals totals;
+  int32_t dtype;                /* FOCUS_BF16                                */
+  int32_t n_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;             /* 64 or 128                                 */
+  float softmax_scale;          /* <= 0: 1/sqrt(head_dim)                    */
+  int32_t mask;                 /* focus_mask                                */
+  int32_t batch;
+  int32_t kmer_uniform;         /* as in focus_attn_desc                     */
+  int64_t n_win;
+  const int32_t* win_ids;       /* [device] or NULL = all windows            */
+  const int32_t* win_seq;       /* [device] layout arrays                    */
+  const int32_t* win_ntok;
+  const int32_t* win_cache_off;
+  const int64_t* win_tok_off;
+  const int32_t* win_kmer;      /* as in focus_attn_desc                     */
+  const int32_t* win_nsum;
+  const int64_t* win_sum_off;
+  const int64_t* sum_tok;
+  const void* q_sum;            /* [sum_rows, n_heads, head_dim]             */
+  int64_t sum_base;             /* global summary index of row 0             */
+  int64_t sum_rows;
+  const void* k;                /* [kv_rows, n_kv_heads, head_dim]           */
+  const void* v;
+  int64_t kv_tok_base;
+  int64_t kv_rows;
+  const void* cache_k;          /* [batch, cache_cap, n_kv_heads, head_dim]  */
+  const void* cache_v;
+  int64_t cache_cap;
+  void* o_sum;                  /* [sum_rows, n_heads, head_dim]             */
+  float* lse_sum;               /* [sum_rows, n_heads] or NULL               */
+  int32_t* err;
+} focus_adapter_desc;
+
+focus_status focus_adapter_attn(const focus_adapter_desc* d, focus_stream_t stream);
+
+/* The whole adapter update of the summary tokens at one layer (eq. focus-attn
+ * with the output projection), over every window of the layout:
+ *     K = hidden W_K, V = hidden W_V               (every token; focus_gemm)
+ *     cache = K, V rows of the summary tokens      (focus_compact_kv)
+ *     Q = hidden[sum_tok] W_Q                      (summary tokens only)
+ *     A = focus_adapter_attn(Q, K, V, cache, mask)
+ *     out = A W_O                                  ([n_summaries, d_model])
+ * hidden [n_tokens, d_model] (global token order); w_q [d_model, H D]; w_k, w_v
+ * [d_model, H_kv D]; w_o [H D, d_model]; all bf16, row-major.  Intermediates
+ * live in the caller's workspace (size from focus_adapter_layer_workspace).
+ * Requirements: d_model a multiple of 128 and of 64; H D and H_kv D multiples of
+ * 128.  Errors: as the calls above. */
+typedef struct {
+  focus_layout_totals totals;
+  int32_t dtype;                /* FOCUS_BF16                                */
+  int32_t n_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;             /* 64 or 128                                 */
+  int32_t d_model;
+  float softmax_scale;          /* <= 0: 1/sqrt(head_dim)                    */
+  int32_t mask;                 /* focus_mask                                */
+  int32_t batch;
+  int32_t kmer_uniform;
+  int32_t reserved;
+  const int32_t* win_seq;       /* [device] layout arrays                    */
+  const int32_t* win_ntok;
+  const int32_t* win_cache_off;
+  const int64_t* win_tok_off;
+  const int32_t* win_kmer;
+  const int32_t* win_nsum;
+  const int64_t* win_sum_off;
+  const int64_t* sum_tok;
+  const void* hidden;           /* [n_tokens, d_model]                       */
+  const void* w_q;
+  const void* w_k;
+  const void* w_v;
+  const void* w_o;
+  void* out;                    /* [n_summaries, d_model]                    */
+  void* workspace;
+  size_t workspace_bytes;
+  int32_t* err;
+} focus_adapter_layer_desc;
+
+size_t focus_adapter_layer_workspace(const focus_adapter_layer_desc* d);
+focus_status focus_adapter_layer(const focus_adapter_layer_desc* d, focus_stream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Projections                                                               */
+/* ------------------------------------------------------------------------ */
+
+/* bf16 matrix product with float32 accumulation, for the projections around
+ * the attention (the FOCUS adapter's W_Q, W_K, W_V, W_O of Appendix A eq.
+ * focus-attn, and the layer's Q/K/V projection):
+ *     C[i, n] = alpha * sum_k A[r(i), k] * B[k, n],  0 <= i < m, 0 <= n < n,
+ *     r(i) = a_rows ? a_rows[i] : i
+ * A, B, C row-major with leading dimensions lda, ldb, ldc (elements).  a_rows
+ * (device, int64) gathers rows of A, e.g. the hidden states of the summary
+ * tokens (sum_tok of focus_layout).  C is bf16 (round to nearest even) or f32.
+ * Requirements: k a multiple of 64, n a multiple of 128, lda and ldb multiples
+ * of 8, A and B 16-byte aligned.  Errors: E_NULL, E_ARG, E_DTYPE,
+ * E_UNSUPPORTED (k or n not a multiple of the tile), E_SHAPE, E_HIP.  A gathered
+ * row outside [0, a_nrows) reads row 0 instead and sets FOCUS_ERR_BOUNDS. */
+typedef struct {
+  int64_t m, n, k;
+  const void* a;                /* [device] bf16, rows of lda elements       */
+  int64_t lda;
+  const int64_t* a_rows;        /* [device][m] row of A for each row of C, or NULL */
+  int64_t a_nrows;              /* rows of A (a_rows entries must be below)  */
+  const void* b;                /* [device] bf16 [k, ldb]                    */
+  int64_t ldb;
+  void* c;                      /* [device] [m, ldc] of c_dtype              */
+  int64_t ldc;
+  int32_t c_dtype;              /* FOCUS_BF16 or FOCUS_F32                   */
+  float alpha;
+  int32_t* err;                 /* optional error word                       */
+} focus_gemm_desc;
+
+focus_status focus_gemm(const focus_gemm_desc* d, focus_stream_t stream);
 
 #ifdef __cplusplus
 }

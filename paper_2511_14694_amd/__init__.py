@@ -23,7 +23,7 @@ from typing import Dict, Optional
 import numpy as np
 import torch
 
-from ._abi import (AttnDesc, CompactDesc, DecodeDesc, FidelityDesc, FocusError, LayoutDesc, LayoutTotals,
+from ._abi import (AdapterDesc, AdapterLayerDesc, AttnDesc, CompactDesc, DecodeDesc, FidelityDesc, FocusError, GemmDesc, LayoutDesc, LayoutTotals,
                    FOCUS_BF16, FOCUS_F32, FOCUS_MASK_CT, FOCUS_MASK_KMER_LOCAL,
                    FOCUS_TOK_BASE, FOCUS_TOK_SUMMARY, FOCUS_STEP_SUMMARY, FOCUS_STEP_WINDOW_END,
                    FOCUS_ERR_CAPACITY, FOCUS_ERR_BOUNDS, FOCUS_ERR_PLAN,
@@ -31,7 +31,8 @@ from ._abi import (AttnDesc, CompactDesc, DecodeDesc, FidelityDesc, FocusError, 
 
 __all__ = ["focus_layout_plan", "focus_layout", "focus_compact_kv", "focus_window_attn",
            "focus_window_attn_workspace", "focus_decode_step", "focus_decode_workspace",
-           "focus_fidelity", "focus_abi_version", "Layout", "LayoutTotals", "FocusError",
+           "focus_fidelity", "focus_gemm", "focus_adapter_attn", "focus_adapter_layer",
+           "focus_adapter_layer_workspace", "focus_abi_version", "Layout", "LayoutTotals", "FocusError",
            "FOCUS_FID_LOGITS", "FOCUS_FID_PROBS", "FOCUS_FID_N",
            "FOCUS_BF16", "FOCUS_F32", "FOCUS_MASK_CT", "FOCUS_MASK_KMER_LOCAL",
            "FOCUS_TOK_BASE", "FOCUS_TOK_SUMMARY", "FOCUS_STEP_SUMMARY", "FOCUS_STEP_WINDOW_END",
@@ -59,6 +60,13 @@ def _ptr(t) -> Optional[int]:
         return None
     if not t.is_contiguous():
         raise ValueError("tensors passed to libfocus must be contiguous")
+    return t.data_ptr()
+
+
+def _ptr_rows(t) -> int:
+    """Pointer of a 2-D tensor with unit column stride (any row stride)."""
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError("expected a 2-D tensor with unit column stride")
     return t.data_ptr()
 
 
@@ -301,3 +309,112 @@ def focus_fidelity(p, q, input_kind: int = FOCUS_FID_LOGITS, cu_pos=None, out=No
     d.cu_pos, d.seq_mean, d.err = _ptr(cu_pos), _ptr(seq_mean), _ptr(err)
     check("focus_fidelity", lib().focus_fidelity(C.byref(d), _stream(stream, p.device)))
     return out, seq_mean
+
+
+def focus_gemm(a, b, out=None, a_rows=None, alpha: float = 1.0, out_dtype=torch.bfloat16, err=None,
+               stream=None):
+    """out[i] = alpha * a[a_rows[i] if a_rows is not None else i] @ b  (bf16 inputs,
+    float32 accumulation).  a [rows, k], b [k, n] bf16 row-major (unit column
+    stride); returns out [m, n] of out_dtype."""
+    if a.dtype != torch.bfloat16 or b.dtype != torch.bfloat16 or a.dim() != 2 or b.dim() != 2:
+        raise ValueError("a and b must be 2-D bfloat16 tensors")
+    if a.stride(1) != 1 or b.stride(1) != 1 or a.shape[1] != b.shape[0]:
+        raise ValueError("a [rows, k] and b [k, n] must be row-major with matching k")
+    if a_rows is not None:
+        a_rows = torch.as_tensor(a_rows, dtype=torch.int64).to(a.device).contiguous()
+    m = a.shape[0] if a_rows is None else a_rows.numel()
+    n = b.shape[1]
+    if out is None:
+        out = torch.empty(m, n, dtype=out_dtype, device=a.device)
+    if tuple(out.shape) != (m, n) or out.stride(1) != 1:
+        raise ValueError("out must be [m, n] row-major")
+    d = GemmDesc()
+    d.m, d.n, d.k = m, n, a.shape[1]
+    d.a, d.lda, d.a_rows, d.a_nrows = _ptr_rows(a), a.stride(0), _ptr(a_rows), a.shape[0]
+    d.b, d.ldb = _ptr_rows(b), b.stride(0)
+    d.c, d.ldc, d.c_dtype = _ptr_rows(out), out.stride(0), _dtype(out)
+    d.alpha = float(alpha)
+    d.err = _ptr(err)
+    check("focus_gemm", lib().focus_gemm(C.byref(d), _stream(stream, a.device)))
+    return out
+
+
+def focus_adapter_attn(lay: Layout, q_sum, k, v, cache_k=None, cache_v=None, o_sum=None, lse_sum=None,
+                       win_ids=None, sum_base: int = 0, kv_tok_base: int = 0, mask: int = FOCUS_MASK_CT,
+                       softmax_scale: float = 0.0, want_lse: bool = True, err=None, stream=None):
+    """FOCUS adapter attention of the summary tokens: q_sum [rows, H, D] (row =
+    global summary index - sum_base), k / v [rows, H_kv, D] (row = token -
+    kv_tok_base), cache [batch, cap, H_kv, D].  Returns (o_sum, lse_sum)."""
+    if o_sum is None:
+        o_sum = torch.empty_like(q_sum)
+    if lse_sum is None and want_lse:
+        lse_sum = torch.empty(q_sum.shape[0], q_sum.shape[1], dtype=torch.float32, device=q_sum.device)
+    if (o_sum.shape != q_sum.shape or q_sum.dtype != k.dtype or k.shape != v.shape
+            or q_sum.shape[2] != k.shape[2]):
+        raise ValueError("adapter attention shapes disagree")
+    d = AdapterDesc()
+    d.totals = lay.totals
+    d.dtype = _dtype(q_sum)
+    d.n_heads, d.head_dim = q_sum.shape[1], q_sum.shape[2]
+    d.n_kv_heads = k.shape[1]
+    d.softmax_scale, d.mask, d.batch = float(softmax_scale), int(mask), lay.batch
+    d.kmer_uniform, d.win_kmer = int(lay.kmer_uniform), _ptr(lay.kmer)
+    d.n_win = 0 if win_ids is None else win_ids.numel()
+    d.win_ids = _ptr(win_ids)
+    for f in ("win_seq", "win_ntok", "win_cache_off", "win_tok_off", "win_nsum", "win_sum_off", "sum_tok"):
+        setattr(d, f, _ptr(lay[f]))
+    d.q_sum, d.sum_base, d.sum_rows = _ptr(q_sum), int(sum_base), q_sum.shape[0]
+    d.k, d.v, d.kv_tok_base, d.kv_rows = _ptr(k), _ptr(v), int(kv_tok_base), k.shape[0]
+    if cache_k is not None:
+        if cache_k.shape != cache_v.shape or cache_k.shape[2:] != k.shape[1:] or cache_k.dtype != k.dtype:
+            raise ValueError("adapter cache shape/dtype does not match k")
+        d.cache_k, d.cache_v, d.cache_cap = _ptr(cache_k), _ptr(cache_v), cache_k.shape[1]
+    d.o_sum, d.lse_sum, d.err = _ptr(o_sum), _ptr(lse_sum), _ptr(err)
+    check("focus_adapter_attn", lib().focus_adapter_attn(C.byref(d), _stream(stream, q_sum.device)))
+    return o_sum, lse_sum
+
+
+def _adapter_layer_desc(lay: Layout, hidden, w_q, w_k, w_v, w_o, n_heads, n_kv_heads, mask, softmax_scale,
+                        out, workspace, err):
+    d = AdapterLayerDesc()
+    d.totals = lay.totals
+    d.dtype = _dtype(hidden)
+    d.n_heads, d.n_kv_heads = int(n_heads), int(n_kv_heads)
+    d.d_model = hidden.shape[1]
+    d.head_dim = w_q.shape[1] // int(n_heads)
+    if (w_q.shape != (d.d_model, n_heads * d.head_dim) or w_k.shape != (d.d_model, n_kv_heads * d.head_dim)
+            or w_v.shape != w_k.shape or w_o.shape != (n_heads * d.head_dim, d.d_model)
+            or hidden.shape[0] != lay.totals.n_tokens):
+        raise ValueError("adapter weight / hidden shapes disagree")
+    d.softmax_scale, d.mask, d.batch = float(softmax_scale), int(mask), lay.batch
+    d.kmer_uniform, d.win_kmer = int(lay.kmer_uniform), _ptr(lay.kmer)
+    for f in ("win_seq", "win_ntok", "win_cache_off", "win_tok_off", "win_nsum", "win_sum_off", "sum_tok"):
+        setattr(d, f, _ptr(lay[f]))
+    d.hidden, d.w_q, d.w_k, d.w_v, d.w_o = _ptr(hidden), _ptr(w_q), _ptr(w_k), _ptr(w_v), _ptr(w_o)
+    d.out = _ptr(out)
+    d.workspace = _ptr(workspace)
+    d.workspace_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    d.err = _ptr(err)
+    return d
+
+
+def focus_adapter_layer_workspace(lay: Layout, hidden, w_q, w_k, w_v, w_o, n_heads: int, n_kv_heads: int) -> int:
+    d = _adapter_layer_desc(lay, hidden, w_q, w_k, w_v, w_o, n_heads, n_kv_heads, FOCUS_MASK_CT, 0.0,
+                            None, None, None)
+    return lib().focus_adapter_layer_workspace(C.byref(d))
+
+
+def focus_adapter_layer(lay: Layout, hidden, w_q, w_k, w_v, w_o, n_heads: int, n_kv_heads: int,
+                        mask: int = FOCUS_MASK_CT, softmax_scale: float = 0.0, out=None, workspace=None,
+                        err=None, stream=None):
+    """FOCUS adapter update of the summary tokens (eq. focus-attn): returns
+    out [n_summaries, d_model] in summary order."""
+    if out is None:
+        out = torch.empty(lay.totals.n_summaries, hidden.shape[1], dtype=hidden.dtype, device=hidden.device)
+    if workspace is None:
+        n = focus_adapter_layer_workspace(lay, hidden, w_q, w_k, w_v, w_o, n_heads, n_kv_heads)
+        workspace = torch.empty(max(n, 256), dtype=torch.uint8, device=hidden.device)
+    d = _adapter_layer_desc(lay, hidden, w_q, w_k, w_v, w_o, n_heads, n_kv_heads, mask, softmax_scale,
+                            out, workspace, err)
+    check("focus_adapter_layer", lib().focus_adapter_layer(C.byref(d), _stream(stream, hidden.device)))
+    return out

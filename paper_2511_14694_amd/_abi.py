@@ -76,7 +76,36 @@ class FidelityDesc(C.Structure):
                 ("p", p), ("q", p), ("out", p), ("cu_pos", p), ("seq_mean", p), ("err", p)]
 
 
-STRUCTS = [LayoutTotals, LayoutDesc, CompactDesc, AttnDesc, DecodeDesc, FidelityDesc]
+class GemmDesc(C.Structure):
+    _fields_ = [("m", i64), ("n", i64), ("k", i64), ("a", p), ("lda", i64), ("a_rows", p),
+                ("a_nrows", i64), ("b", p), ("ldb", i64), ("c", p), ("ldc", i64), ("c_dtype", i32),
+                ("alpha", f32), ("err", p)]
+
+
+class AdapterDesc(C.Structure):
+    _fields_ = [("totals", LayoutTotals), ("dtype", i32), ("n_heads", i32), ("n_kv_heads", i32),
+                ("head_dim", i32), ("softmax_scale", f32), ("mask", i32), ("batch", i32),
+                ("kmer_uniform", i32), ("n_win", i64), ("win_ids", p),
+                ("win_seq", p), ("win_ntok", p), ("win_cache_off", p), ("win_tok_off", p),
+                ("win_kmer", p), ("win_nsum", p), ("win_sum_off", p), ("sum_tok", p),
+                ("q_sum", p), ("sum_base", i64), ("sum_rows", i64),
+                ("k", p), ("v", p), ("kv_tok_base", i64), ("kv_rows", i64),
+                ("cache_k", p), ("cache_v", p), ("cache_cap", i64), ("o_sum", p), ("lse_sum", p),
+                ("err", p)]
+
+
+class AdapterLayerDesc(C.Structure):
+    _fields_ = [("totals", LayoutTotals), ("dtype", i32), ("n_heads", i32), ("n_kv_heads", i32),
+                ("head_dim", i32), ("d_model", i32), ("softmax_scale", f32), ("mask", i32), ("batch", i32),
+                ("kmer_uniform", i32), ("reserved", i32),
+                ("win_seq", p), ("win_ntok", p), ("win_cache_off", p), ("win_tok_off", p), ("win_kmer", p),
+                ("win_nsum", p), ("win_sum_off", p), ("sum_tok", p),
+                ("hidden", p), ("w_q", p), ("w_k", p), ("w_v", p), ("w_o", p), ("out", p),
+                ("workspace", p), ("workspace_bytes", sz), ("err", p)]
+
+
+STRUCTS = [LayoutTotals, LayoutDesc, CompactDesc, AttnDesc, DecodeDesc, FidelityDesc, GemmDesc, AdapterDesc,
+           AdapterLayerDesc]
 
 # name -> (restype, argtypes): every symbol include/focus.h declares
 SYMBOLS = {
@@ -91,6 +120,10 @@ SYMBOLS = {
     "focus_decode_workspace": (sz, [C.POINTER(DecodeDesc)]),
     "focus_decode_step": (i32, [C.POINTER(DecodeDesc), p]),
     "focus_fidelity": (i32, [C.POINTER(FidelityDesc), p]),
+    "focus_gemm": (i32, [C.POINTER(GemmDesc), p]),
+    "focus_adapter_attn": (i32, [C.POINTER(AdapterDesc), p]),
+    "focus_adapter_layer_workspace": (sz, [C.POINTER(AdapterLayerDesc)]),
+    "focus_adapter_layer": (i32, [C.POINTER(AdapterLayerDesc), p]),
 }
 
 

@@ -21,7 +21,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libfocus.so")
-SOURCES = ["api.hip", "layout.hip", "compact.hip", "window_attn.hip", "decode.hip", "fidelity.hip"]
+SOURCES = ["api.hip", "layout.hip", "compact.hip", "window_attn.hip", "decode.hip", "fidelity.hip", "gemm.hip", "adapter.hip"]
 
 ARCH = "gfx950"
 # Packed fp32 VALU ops are kept out of all device code (-packed-fp32-ops); the

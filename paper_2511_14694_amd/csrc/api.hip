@@ -27,6 +27,9 @@ extern "C" int64_t focus_struct_size(int32_t which) {
     case 3: return sizeof(focus_attn_desc);
     case 4: return sizeof(focus_decode_desc);
     case 5: return sizeof(focus_fidelity_desc);
+    case 6: return sizeof(focus_gemm_desc);
+    case 7: return sizeof(focus_adapter_desc);
+    case 8: return sizeof(focus_adapter_layer_desc);
     default: return -1;
   }
 }

@@ -1,0 +1,171 @@
+// bf16 matrix product on the matrix cores (focus_gemm):
+//     C[i, n] = alpha * sum_k A[r(i), k] * B[k, n],   r(i) = a_rows ? a_rows[i] : i
+// with float32 accumulation, for the projections around the attention (the
+// FOCUS adapter's W_Q / W_K / W_V / W_O of eq. focus-attn, and the layer's
+// Q/K/V projection).  a_rows gathers A's rows, so the summary tokens' queries
+// are projected without first copying their hidden states.
+//
+// One workgroup = 4 waves = a 128 x 128 tile of C; each wave owns 64 x 64 as
+// 2 x 2 blocks of v_mfma_f32_32x32x16_bf16.  K advances 64 at a time through
+// LDS, double-buffered, copied global -> LDS directly (global_load_lds, 16 B
+// per lane; the A copy gathers rows per lane).  A is read with ds_read_b128
+// from 128-byte rows whose 16-byte chunks are XOR-swizzled by row; B (row-
+// major [K, N]) is read k-major with the transposing ds_read_b64_tr_b16 from
+// 256-byte rows whose 64-byte granules are XOR-swizzled, as the attention's V.
+#include "common.h"
+
+namespace {
+
+using focus::bf16x4;
+using focus::bf16x8;
+using focus::f32x16;
+
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+typedef __attribute__((address_space(3))) void lds_void;
+
+constexpr int kBM = 128, kBN = 128, kBKk = 64;   // C tile, K step
+constexpr int kThreads = 256;
+constexpr int kGroupM = 16;                      // A row stripes per sweep of B
+constexpr int kARow = kBKk * 2;                  // bytes per A tile row (128)
+constexpr int kBRow = kBN * 2;                   // bytes per B tile row (256)
+constexpr int kATile = kBM * kARow;              // 16 KB
+constexpr int kBTile = kBKk * kBRow;             // 16 KB
+
+__device__ inline int a_off(int r, int c16) { return r * kARow + ((c16 ^ (r & 7)) << 4); }
+__device__ inline int b_off(int r, int byte) { return r * kBRow + (((byte >> 6) ^ (r & 3)) << 6) + (byte & 63); }
+
+__global__ __launch_bounds__(kThreads, 2) void gemm_bf16(focus_gemm_desc d, int64_t m_tiles) {
+  __shared__ __attribute__((aligned(1024))) char abuf0[kATile], abuf1[kATile];
+  __shared__ __attribute__((aligned(1024))) char bbuf0[kBTile], bbuf1[kBTile];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, l32 = lane & 31, g = lane >> 5;
+  // Grouped order: kGroupM row stripes of A sweep every column tile before the
+  // next group starts, so A is read from HBM about once and B (the weights)
+  // stays in the last-level cache.
+  const int64_t n_tiles = d.n / kBN, per_group = (int64_t)kGroupM * n_tiles;
+  const int64_t grp0 = blockIdx.x / per_group, in_grp = blockIdx.x % per_group;
+  const int64_t gm_rows = min((int64_t)kGroupM, m_tiles - grp0 * kGroupM);
+  const int64_t mt = grp0 * kGroupM + in_grp % gm_rows, nt = in_grp / gm_rows;
+  const int64_t m0 = mt * kBM, n0 = nt * kBN;
+  const int wm = (wave & 1) * 64, wn = (wave >> 1) * 64;   // this wave's 64 x 64 in the tile
+
+  // Copy plan: A tile = 16 wave-loads of 1 KB (8 rows x 128 B), 4 per wave;
+  // B tile = 16 wave-loads (4 rows x 256 B), 4 per wave.  Lane p of a row
+  // fetches the global chunk the swizzled layout keeps at its slot.
+  const char* A = reinterpret_cast<const char*>(d.a);
+  const char* B = reinterpret_cast<const char*>(d.b);
+  const int64_t a_ld = d.lda * 2, b_ld = d.ldb * 2;
+  const char* a_src[4];
+  uint32_t b_col[4];
+  int brow[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = (wave * 4 + i) * 8 + (lane >> 3), p = lane & 7;   // A tile row, 16-B slot
+    const int64_t gm = min(m0 + r, d.m - 1);                         // ragged M: repeat the last row
+    int64_t ar = d.a_rows ? d.a_rows[gm] : gm;
+    if (ar < 0 || ar >= d.a_nrows) {
+      focus::raise_err(d.err, FOCUS_ERR_BOUNDS);
+      ar = 0;
+    }
+    a_src[i] = A + ar * a_ld + ((p ^ (r & 7)) << 4);
+    brow[i] = (wave * 4 + i) * 4 + (lane >> 4);                      // B tile row
+    const int pb = lane & 15;                                        // its 16-B slot
+    b_col[i] = (uint32_t)((((pb >> 2) ^ (brow[i] & 3)) * 4 + (pb & 3)) * 16);
+  }
+
+  auto issue = [&](int64_t k0, char* ab, char* bb) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const char* ga = a_src[i] + k0 * 2;
+      __builtin_amdgcn_global_load_lds(ga, (lds_void*)(ab + (wave * 4 + i) * 1024), 16, 0, 0);
+      const char* gb = B + (k0 + brow[i]) * b_ld + n0 * 2 + b_col[i];
+      __builtin_amdgcn_global_load_lds(gb, (lds_void*)(bb + (wave * 4 + i) * 1024), 16, 0, 0);
+    }
+  };
+
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  // transposing-read coordinates: lane = 16 * grp + 4 * ri + bq
+  const int grp = lane >> 4, ri = (lane >> 2) & 3, bq = lane & 3;
+  auto compute = [&](const char* ab, const char* bb) {
+#pragma unroll
+    for (int s = 0; s < kBKk / 16; ++s) {
+      bf16x8 af[2], bf[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) af[i] = *reinterpret_cast<const bf16x8*>(ab + a_off(wm + 32 * i + l32, 2 * s + g));
+      // B operand in the natural k order of the A operand: lane (n, g) holds
+      // B[16 s + 8 g + e][n], e = 0..7.  Each transposing read gives a lane one
+      // column of the 4 rows its quad points at: rows 16 s + 8 g + ri (e < 4),
+      // then 4 further down (e >= 4).
+      const int kb = 16 * s + 8 * (grp >> 1) + ri;
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int col_byte = 2 * (wn + 32 * j + 16 * (grp & 1) + 4 * bq);
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(bb + b_off(kb, col_byte)));
+        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(bb + b_off(kb + 4, col_byte)));
+        bf[j] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+    }
+  };
+
+  const int64_t nk = d.k / kBKk;
+  issue(0, abuf0, bbuf0);
+  __syncthreads();
+  for (int64_t t = 0; t < nk; t += 2) {
+    if (t + 1 < nk) issue((t + 1) * kBKk, abuf1, bbuf1);
+    compute(abuf0, bbuf0);
+    __syncthreads();
+    if (t + 1 >= nk) break;
+    if (t + 2 < nk) issue((t + 2) * kBKk, abuf0, bbuf0);
+    compute(abuf1, bbuf1);
+    __syncthreads();
+  }
+
+  // acc[i][j][v] = C[m0 + wm + 32 i + 8 (v / 4) + 4 g + v % 4][n0 + wn + 32 j + l32]
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int64_t row = m0 + wm + 32 * i + 8 * (v >> 2) + 4 * g + (v & 3);
+      if (row >= d.m) continue;
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int64_t col = n0 + wn + 32 * j + l32;
+        const float x = acc[i][j][v] * d.alpha;
+        if (d.c_dtype == FOCUS_BF16)
+          reinterpret_cast<__bf16*>(d.c)[row * d.ldc + col] = (__bf16)x;
+        else
+          reinterpret_cast<float*>(d.c)[row * d.ldc + col] = x;
+      }
+    }
+}
+
+}  // namespace
+
+extern "C" focus_status focus_gemm(const focus_gemm_desc* d, focus_stream_t stream) {
+  if (!d) return FOCUS_E_NULL;
+  if (d->c_dtype != FOCUS_BF16 && d->c_dtype != FOCUS_F32) return FOCUS_E_DTYPE;
+  if (d->m < 0 || d->n < 0 || d->k < 0 || !(d->alpha == d->alpha)) return FOCUS_E_ARG;
+  if (d->m == 0 || d->n == 0) return FOCUS_OK;
+  if (d->k == 0 || d->k % kBKk || d->n % kBN) return FOCUS_E_UNSUPPORTED;
+  if (!d->a || !d->b || !d->c) return FOCUS_E_NULL;
+  if (d->lda < d->k || d->ldb < d->n || d->ldc < d->n || d->lda % 8 || d->ldb % 8) return FOCUS_E_ARG;
+  if (d->a_nrows < (d->a_rows ? 1 : d->m)) return FOCUS_E_ARG;
+  if (!focus::aligned16(d->a) || !focus::aligned16(d->b) || (reinterpret_cast<uintptr_t>(d->c) & 3u) ||
+      (reinterpret_cast<uintptr_t>(d->a_rows) & 7u))
+    return FOCUS_E_ARG;
+  const int64_t m_tiles = focus::ceil_div(d->m, kBM), n_tiles = d->n / kBN;
+  if (m_tiles * n_tiles > INT32_MAX) return FOCUS_E_SHAPE;
+  hipLaunchKernelGGL(gemm_bf16, dim3((uint32_t)(m_tiles * n_tiles)), dim3(kThreads), 0,
+                     reinterpret_cast<hipStream_t>(stream), *d, m_tiles);
+  return focus::launch_status();
+}

@@ -118,8 +118,23 @@ __device__ inline int v_off(int r, int byte) {
   return r * (D * 2) + ((((byte >> 6) ^ f)) << 6) + (byte & 63);
 }
 
-template <int D, int W, bool KL>
-__global__ __launch_bounds__(64 * W, 2) void attn_bf16(focus_attn_desc d, float sc, int64_t n_pairs, int QT) {
+// Summary-query mode (the FOCUS adapter attention of eq. focus-attn): the
+// queries of a window are its summary tokens only; query slot j is summary
+// win_sum_off[w] + j at window row sum_tok[...] - win_tok_off[w], and q / o /
+// lse rows are indexed by global summary index - base.
+struct SumQ {
+  const int32_t* win_nsum;
+  const int64_t* win_sum_off;
+  const int64_t* sum_tok;
+  const void* q;
+  void* o;
+  float* lse;
+  int64_t base, rows;
+};
+
+template <int D, int W, bool KL, bool SQ>
+__global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_desc d, float sc, int64_t n_pairs, int QT,
+                                                       SumQ sq) {
   using C = Cfg<D, W>;
   // Two K and two V tile buffers as separate arrays, referenced statically by
   // a loop unrolled by two: the compiler can then tell a tile being read from
@@ -137,17 +152,33 @@ __global__ __launch_bounds__(64 * W, 2) void attn_bf16(focus_attn_desc d, float 
   }
   const int T = d.win_ntok[gw];
   const int q0 = it.qt * C::kBQ;
-  if (q0 >= T) return;
+  int nq = T;          // query slots of the window
+  int64_t s0 = 0;      // summary mode: the window's first summary
+  if constexpr (SQ) {
+    nq = sq.win_nsum[gw];
+    s0 = sq.win_sum_off[gw];
+  }
+  if (q0 >= nq) return;
   const int Cw = d.win_cache_off[gw];
   const int b = d.win_seq[gw];
   const int64_t tok0 = d.win_tok_off[gw] - d.qkv_tok_base;
-  if (b < 0 || b >= d.batch || Cw < 0 || Cw > d.cache_cap || tok0 < 0 || tok0 + T > d.qkv_rows) {
+  if (b < 0 || b >= d.batch || Cw < 0 || Cw > d.cache_cap || tok0 < 0 || tok0 + T > d.qkv_rows ||
+      (SQ && (nq > T || s0 < sq.base || s0 + nq > sq.base + sq.rows))) {
     if (tid == 0) focus::raise_err(d.err, FOCUS_ERR_BOUNDS);
     return;
   }
+  // window row of query slot j (clamped to the last slot)
+  auto qpos = [&](int j) -> int {
+    j = min(j, nq - 1);
+    if constexpr (SQ) {
+      const int64_t r = sq.sum_tok[s0 + j] - d.win_tok_off[gw];
+      return (int)(r < 0 ? 0 : r >= T ? T - 1 : r);
+    }
+    return j;
+  };
   const int H = d.n_heads, Hkv = d.n_kv_heads, h = it.h;
   const int hk = h / (H / Hkv);
-  const int nwk = min(T, q0 + C::kBQ);  // window keys any query of this tile can see
+  const int nwk = qpos(q0 + C::kBQ - 1) + 1;  // window keys any query of this tile can see
   // C(t): keys are visited as nct tiles of cache rows [0, Cw) followed by nwt
   // tiles of window rows [0, nwk); only the last tile of each phase is partial.
   // k-mer-local: the first nct tiles hold the summary list [carried boundary
@@ -162,33 +193,36 @@ __global__ __launch_bounds__(64 * W, 2) void attn_bf16(focus_attn_desc d, float 
       return;
     }
     nsum = kw > 0 ? (T + kw) / (kw + 1) : 0;
-    tw0 = kw > 0 ? (q0 / (kw + 1)) * (kw + 1) / C::kBK : 0;
+    // first row of the k-mer of the tile's first query (summary j closes k-mer j)
+    const int first_kmer = SQ ? q0 : (kw > 0 ? q0 / (kw + 1) : 0);
+    tw0 = kw > 0 ? first_kmer * (kw + 1) / C::kBK : 0;
   }
   const int nct = KL ? (nsum + C::kBK) / C::kBK : (Cw + C::kBK - 1) / C::kBK;
   const int nwt = (nwk + C::kBK - 1) / C::kBK - tw0;
   const int ntiles = nct + nwt;
 
   const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, g = lane >> 5;
-  const int qi = q0 + wave * 32 + l32;  // this lane's query row inside the window
-  const int wq_lo = q0 + wave * 32, wq_hi = wq_lo + 31;
-  const bool wave_live = wq_lo < T;
+  const int js = q0 + wave * 32 + l32;  // this lane's query slot
+  const int qi = SQ ? qpos(js) : js;     // and its row inside the window
+  const int wq_lo = qpos(q0 + wave * 32), wq_hi = SQ ? qpos(q0 + wave * 32 + 31) : wq_lo + 31;
+  const bool wave_live = q0 + wave * 32 < nq;
   // k-mer-local: this lane's k-mer index jq inside the window and that
   // k-mer's first row qlo; klo_w: first row of the wave's first k-mer.
   int jq = 0, qlo = 0, klo_w = 0;
   if constexpr (KL) {
     if (kw > 0) {
-      jq = qi / (kw + 1);
+      jq = SQ ? min(js, nq - 1) : qi / (kw + 1);
       qlo = jq * (kw + 1);
-      klo_w = wq_lo / (kw + 1) * (kw + 1);
+      klo_w = (SQ ? min(q0 + wave * 32, nq - 1) : wq_lo / (kw + 1)) * (kw + 1);
     }
   }
 
   // Q^T as the B operand: lane holds query l32, head_dim [16s + 8g, 16s + 8g + 8).
   bf16x8 qf[C::kKsteps];
   {
-    const int64_t qrow = tok0 + min(qi, T - 1);
+    const int64_t qrow = SQ ? s0 + min(js, nq - 1) - sq.base : tok0 + min(qi, T - 1);
     const bf16x8* qp = reinterpret_cast<const bf16x8*>(
-        reinterpret_cast<const __bf16*>(d.q) + (qrow * H + h) * D);
+        reinterpret_cast<const __bf16*>(SQ ? sq.q : d.q) + (qrow * H + h) * D);
 #pragma unroll
     for (int s = 0; s < C::kKsteps; ++s) qf[s] = qp[2 * s + g];
   }
@@ -372,10 +406,10 @@ __global__ __launch_bounds__(64 * W, 2) void attn_bf16(focus_attn_desc d, float 
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
-  if (qi < T) {
+  if (SQ ? js < nq : qi < T) {
     const float inv = 1.f / l_tot;
-    const int64_t orow = tok0 + qi;
-    __bf16* op = reinterpret_cast<__bf16*>(d.o) + (orow * H + h) * D;
+    const int64_t orow = SQ ? s0 + js - sq.base : tok0 + qi;
+    __bf16* op = reinterpret_cast<__bf16*>(SQ ? sq.o : d.o) + (orow * H + h) * D;
 #pragma unroll
     for (int dt = 0; dt < C::kDtiles; ++dt)
 #pragma unroll
@@ -386,14 +420,15 @@ __global__ __launch_bounds__(64 * W, 2) void attn_bf16(focus_attn_desc d, float 
         w.y = focus::pack_bf16x2(oacc[dt][4 * v4 + 2] * inv, oacc[dt][4 * v4 + 3] * inv);
         *reinterpret_cast<uint2*>(op + 32 * dt + 8 * v4 + 4 * g) = w;
       }
-    if (g == 0 && d.lse) d.lse[orow * H + h] = (m_run + log2f(l_tot)) * kLn2;
+    float* lse = SQ ? sq.lse : d.lse;
+    if (g == 0 && lse) lse[orow * H + h] = (m_run + log2f(l_tot)) * kLn2;
   }
 }
 
 // ----------------------------------------------------------------- f32 VALU
 
 template <int D, bool KL>
-__global__ __launch_bounds__(256) void attn_f32(focus_attn_desc d, float sc, int64_t n_pairs, int QT) {
+__global__ __launch_bounds__(256) void attn_f32(focus_attn_desc d, float sc, int64_t n_pairs, int QT, SumQ) {
   constexpr int kBQ = 64, kBK = 32, kF4 = D / 4, kPer = D / 16;  // float4 per row / per lane
   __shared__ float4 ks[kBK][kF4];
   __shared__ float4 vs[kBK][kF4];
@@ -555,12 +590,12 @@ extern "C" focus_status focus_window_attn(const focus_attn_desc* d, focus_stream
   if (blocks * threads >= ((int64_t)1 << 32) || qt > INT32_MAX) return FOCUS_E_SHAPE;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const dim3 grid((uint32_t)blocks), block(threads);
-#define FOCUS_ATTN_LAUNCH(KERNEL) hipLaunchKernelGGL(KERNEL, grid, block, 0, s, *d, sc, n_pairs, (int)qt)
+#define FOCUS_ATTN_LAUNCH(KERNEL) hipLaunchKernelGGL(KERNEL, grid, block, 0, s, *d, sc, n_pairs, (int)qt, SumQ{})
   if (d->dtype == FOCUS_BF16) {
     if (d->head_dim == 128) {
-      if (kl) FOCUS_ATTN_LAUNCH((attn_bf16<128, kBf16WavesKL, true>)); else FOCUS_ATTN_LAUNCH((attn_bf16<128, kBf16Waves, false>));
+      if (kl) FOCUS_ATTN_LAUNCH((attn_bf16<128, kBf16WavesKL, true, false>)); else FOCUS_ATTN_LAUNCH((attn_bf16<128, kBf16Waves, false, false>));
     } else {
-      if (kl) FOCUS_ATTN_LAUNCH((attn_bf16<64, kBf16WavesKL, true>)); else FOCUS_ATTN_LAUNCH((attn_bf16<64, kBf16Waves, false>));
+      if (kl) FOCUS_ATTN_LAUNCH((attn_bf16<64, kBf16WavesKL, true, false>)); else FOCUS_ATTN_LAUNCH((attn_bf16<64, kBf16Waves, false, false>));
     }
   } else {
     if (d->head_dim == 128) {
@@ -570,5 +605,78 @@ extern "C" focus_status focus_window_attn(const focus_attn_desc* d, focus_stream
     }
   }
 #undef FOCUS_ATTN_LAUNCH
+  return focus::launch_status();
+}
+
+// FOCUS adapter attention (Appendix A eq. focus-attn): the summary tokens of
+// every listed window attend over [cache ; window] under C(t) or the
+// k-mer-local rule; one wave of 32 summary slots per (window, head).
+extern "C" focus_status focus_adapter_attn(const focus_adapter_desc* a, focus_stream_t stream) {
+  if (!a) return FOCUS_E_NULL;
+  if (a->dtype != FOCUS_BF16) return a->dtype == FOCUS_F32 ? FOCUS_E_UNSUPPORTED : FOCUS_E_DTYPE;
+  if (a->mask != FOCUS_MASK_CT && a->mask != FOCUS_MASK_KMER_LOCAL) return FOCUS_E_ARG;
+  if (a->mask == FOCUS_MASK_KMER_LOCAL && !a->win_kmer && a->kmer_uniform < 0) return FOCUS_E_ARG;
+  if (a->n_heads <= 0 || a->n_kv_heads <= 0 || a->batch < 0 || a->cache_cap < 0 || a->kv_rows < 0 ||
+      a->sum_rows < 0 || (a->win_ids && a->n_win < 0) || !(a->softmax_scale == a->softmax_scale))
+    return FOCUS_E_ARG;
+  if (a->head_dim != 64 && a->head_dim != 128) return FOCUS_E_UNSUPPORTED;
+  if (a->n_heads % a->n_kv_heads) return FOCUS_E_SHAPE;
+  const focus_layout_totals& t = a->totals;
+  if (t.n_windows < 0 || t.max_window_summaries < 0 || t.max_window_cache < 0) return FOCUS_E_SHAPE;
+  const int64_t nwl = a->win_ids ? a->n_win : t.n_windows;
+  if (nwl == 0 || t.max_window_summaries == 0) return FOCUS_OK;
+  if (!a->win_seq || !a->win_ntok || !a->win_cache_off || !a->win_tok_off || !a->win_nsum ||
+      !a->win_sum_off || !a->sum_tok || !a->q_sum || !a->k || !a->v || !a->o_sum)
+    return FOCUS_E_NULL;
+  if (t.max_window_cache > 0 && (!a->cache_k || !a->cache_v)) return FOCUS_E_NULL;
+  if (!focus::aligned16(a->q_sum) || !focus::aligned16(a->k) || !focus::aligned16(a->v) ||
+      !focus::aligned16(a->o_sum) || !focus::aligned16(a->cache_k) || !focus::aligned16(a->cache_v) ||
+      (reinterpret_cast<uintptr_t>(a->lse_sum) & 3u))
+    return FOCUS_E_ARG;
+  if (!a->win_ids && t.max_window_cache > a->cache_cap) return FOCUS_E_CAPACITY;
+
+  focus_attn_desc d = {};
+  d.totals = t;
+  d.dtype = a->dtype;
+  d.n_heads = a->n_heads;
+  d.n_kv_heads = a->n_kv_heads;
+  d.head_dim = a->head_dim;
+  d.softmax_scale = a->softmax_scale;
+  d.mask = a->mask;
+  d.batch = a->batch;
+  d.kmer_uniform = a->kmer_uniform;
+  d.n_win = a->n_win;
+  d.win_ids = a->win_ids;
+  d.win_seq = a->win_seq;
+  d.win_ntok = a->win_ntok;
+  d.win_cache_off = a->win_cache_off;
+  d.win_tok_off = a->win_tok_off;
+  d.win_kmer = a->win_kmer;
+  d.k = a->k;
+  d.v = a->v;
+  d.qkv_tok_base = a->kv_tok_base;
+  d.qkv_rows = a->kv_rows;
+  d.cache_k = a->cache_k;
+  d.cache_v = a->cache_v;
+  d.cache_cap = a->cache_cap;
+  d.err = a->err;
+  const SumQ sq = {a->win_nsum, a->win_sum_off, a->sum_tok, a->q_sum, a->o_sum, a->lse_sum, a->sum_base, a->sum_rows};
+
+  const float scale = a->softmax_scale > 0.f ? a->softmax_scale : 1.0f / sqrtf((float)a->head_dim);
+  const float sc = scale * kLog2e;
+  const int64_t n_pairs = nwl * a->n_heads;
+  const int64_t qt = focus::ceil_div(t.max_window_summaries, 32);
+  const int64_t blocks = focus::ceil_div(n_pairs, focus::kXcds) * focus::kXcds * qt;
+  if (blocks * 64 >= ((int64_t)1 << 32) || qt > INT32_MAX) return FOCUS_E_SHAPE;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const dim3 grid((uint32_t)blocks), block(64);
+  const bool kl = a->mask == FOCUS_MASK_KMER_LOCAL;
+#define FOCUS_SQ_LAUNCH(KERNEL) hipLaunchKernelGGL(KERNEL, grid, block, 0, s, d, sc, n_pairs, (int)qt, sq)
+  if (a->head_dim == 128) {
+    if (kl) FOCUS_SQ_LAUNCH((attn_bf16<128, 1, true, true>)); else FOCUS_SQ_LAUNCH((attn_bf16<128, 1, false, true>));
+  } else {
+    if (kl) FOCUS_SQ_LAUNCH((attn_bf16<64, 1, true, true>)); else FOCUS_SQ_LAUNCH((attn_bf16<64, 1, false, true>));
+  }
+#undef FOCUS_SQ_LAUNCH
   return focus::launch_status();
 }

@@ -137,3 +137,12 @@ def test_causality_and_windows_without_summaries(mask):
         hid2[t + 1:] += rng.standard_normal((n - t - 1, d))
         out2 = AD.adapter_layer(lay, hid2, *w, H, H, mask)
         np.testing.assert_allclose(out2[:s + 1], out[:s + 1], rtol=1e-12, atol=1e-12)
+
+
+def test_round_bf16_matches_torch():
+    import torch
+    rng = np.random.default_rng(11)
+    x = np.concatenate([rng.standard_normal(10000) * 10.0 ** rng.integers(-8, 8, 10000),
+                        [0.0, -0.0, 1.0, 1.00390625, 1.01171875, 65504.0, 3e38]])
+    want = torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(AD.round_bf16(x), want)

@@ -171,9 +171,9 @@ FIDELITY_MUTATIONS = [
 
 ADAPTER_MUTATIONS = [
     ("summary rows shifted", 'rows = layout["sum_tok"][s0:s0 + B] - t0', 'rows = layout["sum_tok"][s0:s0 + B] - t0 - 1'),
-    ("no output projection", "return o.reshape(len(q_sum), n_heads * D) @ w_o",
-     "return o.reshape(len(q_sum), n_heads * D)"),
-    ("queries of the wrong tokens", 'hidden[layout["sum_tok"]] @ w_q', 'hidden[layout["sum_tok"] - 1] @ w_q'),
+    ("no output projection", "return st(o.reshape(n_sum, n_heads * D)) @ w_o",
+     "return st(o.reshape(n_sum, n_heads * D))"),
+    ("queries of the wrong tokens", 'for s in sums]] @ w_q)', 'for s in sums][::-1]] @ w_q)'),
     ("k-mer-local rule ignored", 'if mask == "kmer_local":\n        return A.kmer_local_window_visibility(layout, w)',
      'if mask == "kmer_local":\n        return A.window_visibility(int(layout["win_ntok"][w]), int(layout["win_cache_off"][w]))'),
 ]
