@@ -17,12 +17,14 @@ import oracle.adapter
 import oracle.attention
 import oracle.decode
 import oracle.fidelity
+import oracle.projection
 import oracle.layout
 import test_oracle_adapter as TAD
 import test_oracle_attention as TA
 import test_oracle_decode as TD
 import test_oracle_fidelity as TF
 import test_oracle_kmer_local as TK
+import test_oracle_projection as TP
 import test_oracle_layout as TL
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -96,6 +98,17 @@ def _adapter_pins():
     TAD.test_grouped_kv_heads_equal_repeated_heads()
     for mask in ("ct", "kmer_local"):
         TAD.test_causality_and_windows_without_summaries(mask)
+
+
+def _projection_pins():
+    TP.test_norm_and_identity()
+    TP.test_two_dims_angle_is_the_position()
+    for shift in (1, 100):
+        TP.test_relative_positions(shift)
+    TP.test_projection_without_rotation_and_positions()
+    TP.test_store_bf16_matches_torch()
+    TP.test_second_pair_frequency()
+    TP.test_projection_rotates_at_the_stream_position()
 
 
 def _decode_pins():
@@ -179,6 +192,15 @@ ADAPTER_MUTATIONS = [
 ]
 
 
+PROJECTION_MUTATIONS = [
+    ("rotation the wrong way", "out[..., 1::2] = e * s + o * c", "out[..., 1::2] = -e * s + o * c"),
+    ("frequency exponent without the 2", "theta ** (-2.0 * i / D)", "theta ** (-1.0 * i / D)"),
+    ("value heads from the key columns", "v = y[:, (n_heads + n_kv_heads) * D:]",
+     "v = y[:, n_heads * D:(n_heads + 2 * n_kv_heads) * D][:, :n_kv_heads * D]"),
+    ("positions off by one", 'pos = layout["tok_pos"][rows]', 'pos = layout["tok_pos"][rows] + 1'),
+]
+
+
 def _expect_caught(monkeypatch, pins, patches):
     for mod_obj, attr, value in patches:
         monkeypatch.setattr(mod_obj, attr, value)
@@ -222,7 +244,14 @@ def test_adapter_mutations_are_caught(monkeypatch, name, old, new):
     _expect_caught(monkeypatch, _adapter_pins, [(TAD, "AD", mut)])
 
 
+@pytest.mark.parametrize("name,old,new", PROJECTION_MUTATIONS, ids=[m[0] for m in PROJECTION_MUTATIONS])
+def test_projection_mutations_are_caught(monkeypatch, name, old, new):
+    mut = _mutant(oracle.projection, old, new)
+    _expect_caught(monkeypatch, _projection_pins, [(TP, "P", mut)])
+
+
 def test_unmutated_pins_pass():
+    _projection_pins()
     _adapter_pins()
     _fidelity_pins()
     _layout_pins()
