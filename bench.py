@@ -19,8 +19,9 @@ Also reported on the same JSON line:
   secondary     compaction and decode (batch 16 at ~1 Mb) HBM rates, the dense
                 32 kb causal point, streaming (one window per call) prefill, and
                 the same 1 Mb prefill under the k-mer-local mask (HBM-bound), the
-                fidelity metrics over 1 M positions (HBM-bound), and the FOCUS
-                adapter update of the summary tokens at 1 Mb (d_model 4096)
+                fidelity metrics over 1 M positions (HBM-bound), the FOCUS
+                adapter update of the summary tokens at 1 Mb (d_model 4096), and
+                the fused Q/K/V projection + RoPE + cache write at 1 Mb
 """
 
 from __future__ import annotations
@@ -411,6 +412,38 @@ def secondary_adapter(torch, F, fw, reps=3, d_model=4096):
                                                     "frac_mfma": attn_flops / (attn_ms * 1e-3) / PEAK_BF16_FLOPS}}
 
 
+def secondary_qkv_projection(torch, F, fw, reps=3, d_model=4096):
+    """The layer's Q/K/V projection at 1 Mb (d_model 4096 -> 32 + 2 x 32 heads
+    of 128) with rotary positions at the augmented-stream index and the summary
+    K/V written straight into the cache (no separate compaction pass)."""
+    w = fw.WORKLOADS["prefill_1mb"]
+    H, Hkv, D = w.heads, w.kv_heads, w.head_dim
+    seq = [w.seq_nt] * w.batch
+    km = fw.kmer_draw(w)
+    tot = F.focus_layout_plan(seq, w.window_nt, km)
+    lay = F.focus_layout(tot, seq, w.window_nt, km, device="cuda:0")
+    hid = fw.randn((tot.n_tokens, d_model), "bf16", fw.BASE_SEED + 1, "cuda:0")
+    wqkv = (fw.randn((d_model, (H + 2 * Hkv) * D), "f32", 5, "cuda:0") / np.sqrt(d_model)).to(torch.bfloat16)
+    q = torch.empty(tot.n_tokens, H, D, dtype=torch.bfloat16, device="cuda:0")
+    k = torch.empty(tot.n_tokens, Hkv, D, dtype=torch.bfloat16, device="cuda:0")
+    v = torch.empty_like(k)
+    ck = torch.empty(w.batch, max(tot.max_cache_per_seq, 1), Hkv, D, dtype=torch.bfloat16, device="cuda:0")
+    cv = torch.empty_like(ck)
+    run = lambda: F.focus_qkv_project(lay, hid, wqkv, H, Hkv, 10000.0, q=q, k=k, v=v, cache_k=ck, cache_v=cv)  # noqa
+    run()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    flops = 2 * tot.n_tokens * d_model * (H + 2 * Hkv) * D
+    return {"workload": f"prefill_1mb layout, d_model {d_model} -> ({H} + 2 x {Hkv}) x {D}, RoPE theta 1e4, "
+                        "summary K/V written to the cache in the epilogue",
+            "ms": ms, "tflops": flops / ms / 1e9, "frac_mfma": flops / (ms * 1e-3) / PEAK_BF16_FLOPS}
+
+
 def secondary_streaming(torch, F, s, n_windows=200):
     """Streaming prefill: one window per call (last n_windows windows)."""
     lay = s["lay"]
@@ -532,6 +565,9 @@ def main():
         torch.cuda.empty_cache()
         log("secondary: FOCUS adapter layer")
         sec["adapter_1mb"] = secondary_adapter(torch, F, fw)
+        torch.cuda.empty_cache()
+        log("secondary: fused Q/K/V projection")
+        sec["qkv_projection_1mb"] = secondary_qkv_projection(torch, F, fw)
         result["secondary"] = sec
     elif not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(torch, s, args.cpu_budget)

@@ -91,7 +91,7 @@ int32_t focus_abi_version(void);
 const char* focus_status_str(focus_status s);
 /* sizeof of the descriptor structs below, in declaration order
  * (0 totals, 1 layout, 2 compact, 3 attn, 4 decode, 5 fidelity, 6 gemm,
- * 7 adapter, 8 adapter layer); -1 otherwise.
+ * 7 adapter, 8 adapter layer, 9 qkv projection); -1 otherwise.
  * Lets a binding check its mirror of the structs. */
 int64_t focus_struct_size(int32_t which);
 
@@ -514,6 +514,54 @@ typedef struct {
 } focus_gemm_desc;
 
 focus_status focus_gemm(const focus_gemm_desc* d, focus_stream_t stream);
+
+/* The layer's Q/K/V projection with FOCUS-aware rotary positions and the
+ * compaction fused into its store (the step before the hot path; App. A: the
+ * compression is effected by which K/V rows are retained):
+ *     [Q | K | V] = hidden W_qkv          (rows = tokens tok_base .. +n_rows)
+ *     Q, K rotated by RoPE at tok_pos[t], the token's index in its sequence's
+ *     augmented stream (summary tokens hold real positions, Sec. 3.2 / App. A):
+ *     pairs (2i, 2i+1) of each head turn by tok_pos * theta^(-2i/D)
+ *     K, V rows of summary tokens are also written to cache row tok_kmer[t]
+ *     of sequence win_seq[tok_win[t]], and cache_len raised past it.
+ * w_qkv [d_model, (H + 2 H_kv) D] holds the Q heads, then the K heads, then the
+ * V heads; q [n_rows, H, D], k / v [n_rows, H_kv, D]; all bf16 (float32
+ * accumulation and rotation, then rounding).  rope_theta <= 0 skips the
+ * rotation.  cache_k NULL skips the cache write.  Requirements: (H + 2 H_kv) D
+ * a multiple of 128, d_model a multiple of 64.  Errors: E_NULL, E_ARG, E_DTYPE,
+ * E_SHAPE, E_UNSUPPORTED (f32, tile multiples), E_CAPACITY (whole layout and
+ * cache_cap < max_cache_per_seq), E_HIP; a cache row outside the cache is
+ * skipped with FOCUS_ERR_CAPACITY. */
+typedef struct {
+  focus_layout_totals totals;
+  int32_t dtype;                /* FOCUS_BF16                                */
+  int32_t n_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;             /* 64 or 128                                 */
+  int32_t d_model;
+  int32_t batch;
+  float rope_theta;             /* RoPE base, > 1; <= 0: no rotation         */
+  int32_t reserved;
+  const int32_t* tok_pos;       /* [device] layout arrays                    */
+  const uint8_t* tok_kind;
+  const int32_t* tok_kmer;
+  const int32_t* tok_win;
+  const int32_t* win_seq;
+  int64_t tok_base;             /* global token of hidden row 0              */
+  int64_t n_rows;
+  const void* hidden;           /* [n_rows, d_model]                         */
+  const void* w_qkv;            /* [d_model, (H + 2 H_kv) D]                 */
+  void* q;                      /* [n_rows, H, D]                            */
+  void* k;                      /* [n_rows, H_kv, D]                         */
+  void* v;
+  void* cache_k;                /* [batch, cache_cap, H_kv, D] or NULL       */
+  void* cache_v;
+  int64_t cache_cap;
+  int32_t* cache_len;           /* [device][batch] or NULL                   */
+  int32_t* err;
+} focus_qkv_desc;
+
+focus_status focus_qkv_project(const focus_qkv_desc* d, focus_stream_t stream);
 
 #ifdef __cplusplus
 }

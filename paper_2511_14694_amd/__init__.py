@@ -23,7 +23,7 @@ from typing import Dict, Optional
 import numpy as np
 import torch
 
-from ._abi import (AdapterDesc, AdapterLayerDesc, AttnDesc, CompactDesc, DecodeDesc, FidelityDesc, FocusError, GemmDesc, LayoutDesc, LayoutTotals,
+from ._abi import (AdapterDesc, AdapterLayerDesc, AttnDesc, CompactDesc, DecodeDesc, FidelityDesc, FocusError, GemmDesc, LayoutDesc, LayoutTotals, QkvDesc,
                    FOCUS_BF16, FOCUS_F32, FOCUS_MASK_CT, FOCUS_MASK_KMER_LOCAL,
                    FOCUS_TOK_BASE, FOCUS_TOK_SUMMARY, FOCUS_STEP_SUMMARY, FOCUS_STEP_WINDOW_END,
                    FOCUS_ERR_CAPACITY, FOCUS_ERR_BOUNDS, FOCUS_ERR_PLAN,
@@ -32,7 +32,7 @@ from ._abi import (AdapterDesc, AdapterLayerDesc, AttnDesc, CompactDesc, DecodeD
 __all__ = ["focus_layout_plan", "focus_layout", "focus_compact_kv", "focus_window_attn",
            "focus_window_attn_workspace", "focus_decode_step", "focus_decode_workspace",
            "focus_fidelity", "focus_gemm", "focus_adapter_attn", "focus_adapter_layer",
-           "focus_adapter_layer_workspace", "focus_abi_version", "Layout", "LayoutTotals", "FocusError",
+           "focus_adapter_layer_workspace", "focus_qkv_project", "focus_abi_version", "Layout", "LayoutTotals", "FocusError",
            "FOCUS_FID_LOGITS", "FOCUS_FID_PROBS", "FOCUS_FID_N",
            "FOCUS_BF16", "FOCUS_F32", "FOCUS_MASK_CT", "FOCUS_MASK_KMER_LOCAL",
            "FOCUS_TOK_BASE", "FOCUS_TOK_SUMMARY", "FOCUS_STEP_SUMMARY", "FOCUS_STEP_WINDOW_END",
@@ -418,3 +418,36 @@ def focus_adapter_layer(lay: Layout, hidden, w_q, w_k, w_v, w_o, n_heads: int, n
                             out, workspace, err)
     check("focus_adapter_layer", lib().focus_adapter_layer(C.byref(d), _stream(stream, hidden.device)))
     return out
+
+
+def focus_qkv_project(lay: Layout, hidden, w_qkv, n_heads: int, n_kv_heads: int, rope_theta: float = 10000.0,
+                      tok_base: int = 0, q=None, k=None, v=None, cache_k=None, cache_v=None, cache_len=None,
+                      err=None, stream=None):
+    """[Q | K | V] = hidden @ w_qkv with RoPE at the tokens' augmented-stream
+    positions; summary K/V rows also written to the cache.  Returns (q, k, v)."""
+    rows, d_model = hidden.shape
+    D = w_qkv.shape[1] // (n_heads + 2 * n_kv_heads)
+    if w_qkv.shape != (d_model, (n_heads + 2 * n_kv_heads) * D) or hidden.dtype != w_qkv.dtype:
+        raise ValueError("w_qkv must be [d_model, (H + 2 H_kv) D] of hidden's dtype")
+    mk = lambda h: torch.empty(rows, h, D, dtype=hidden.dtype, device=hidden.device)   # noqa: E731
+    q = mk(n_heads) if q is None else q
+    k = mk(n_kv_heads) if k is None else k
+    v = mk(n_kv_heads) if v is None else v
+    if q.shape != (rows, n_heads, D) or k.shape != (rows, n_kv_heads, D) or v.shape != k.shape:
+        raise ValueError("q / k / v shapes")
+    d = QkvDesc()
+    d.totals = lay.totals
+    d.dtype = _dtype(hidden)
+    d.n_heads, d.n_kv_heads, d.head_dim, d.d_model, d.batch = int(n_heads), int(n_kv_heads), D, d_model, lay.batch
+    d.rope_theta = float(rope_theta)
+    for f in ("tok_pos", "tok_kind", "tok_kmer", "tok_win", "win_seq"):
+        setattr(d, f, _ptr(lay[f]))
+    d.tok_base, d.n_rows = int(tok_base), rows
+    d.hidden, d.w_qkv, d.q, d.k, d.v = _ptr(hidden), _ptr(w_qkv), _ptr(q), _ptr(k), _ptr(v)
+    if cache_k is not None:
+        if cache_k.shape != cache_v.shape or cache_k.shape[2:] != (n_kv_heads, D):
+            raise ValueError("cache shape")
+        d.cache_k, d.cache_v, d.cache_cap = _ptr(cache_k), _ptr(cache_v), cache_k.shape[1]
+    d.cache_len, d.err = _ptr(cache_len), _ptr(err)
+    check("focus_qkv_project", lib().focus_qkv_project(C.byref(d), _stream(stream, hidden.device)))
+    return q, k, v

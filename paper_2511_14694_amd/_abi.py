@@ -104,8 +104,17 @@ class AdapterLayerDesc(C.Structure):
                 ("workspace", p), ("workspace_bytes", sz), ("err", p)]
 
 
+class QkvDesc(C.Structure):
+    _fields_ = [("totals", LayoutTotals), ("dtype", i32), ("n_heads", i32), ("n_kv_heads", i32),
+                ("head_dim", i32), ("d_model", i32), ("batch", i32), ("rope_theta", f32), ("reserved", i32),
+                ("tok_pos", p), ("tok_kind", p), ("tok_kmer", p), ("tok_win", p), ("win_seq", p),
+                ("tok_base", i64), ("n_rows", i64), ("hidden", p), ("w_qkv", p),
+                ("q", p), ("k", p), ("v", p), ("cache_k", p), ("cache_v", p), ("cache_cap", i64),
+                ("cache_len", p), ("err", p)]
+
+
 STRUCTS = [LayoutTotals, LayoutDesc, CompactDesc, AttnDesc, DecodeDesc, FidelityDesc, GemmDesc, AdapterDesc,
-           AdapterLayerDesc]
+           AdapterLayerDesc, QkvDesc]
 
 # name -> (restype, argtypes): every symbol include/focus.h declares
 SYMBOLS = {
@@ -124,6 +133,7 @@ SYMBOLS = {
     "focus_adapter_attn": (i32, [C.POINTER(AdapterDesc), p]),
     "focus_adapter_layer_workspace": (sz, [C.POINTER(AdapterLayerDesc)]),
     "focus_adapter_layer": (i32, [C.POINTER(AdapterLayerDesc), p]),
+    "focus_qkv_project": (i32, [C.POINTER(QkvDesc), p]),
 }
 
 

@@ -34,7 +34,100 @@ constexpr int kBTile = kBKk * kBRow;             // 16 KB
 __device__ inline int a_off(int r, int c16) { return r * kARow + ((c16 ^ (r & 7)) << 4); }
 __device__ inline int b_off(int r, int byte) { return r * kBRow + (((byte >> 6) ^ (r & 3)) << 6) + (byte & 63); }
 
-__global__ __launch_bounds__(kThreads, 2) void gemm_bf16(focus_gemm_desc d, int64_t m_tiles) {
+// Epilogues: col(c) is evaluated once per column a lane stores; the call
+// operator once per element of C with its row, column, float32 value, (kPair)
+// the value of its column partner col ^ 1, and the column's col(c).
+
+// C = alpha * A B, stored as bf16 or f32.
+struct PlainEpi {
+  static constexpr bool kPair = false;
+  struct Col {};
+  void* c;
+  int64_t ldc;
+  int32_t c_dtype;
+  float alpha;
+  __device__ Col col(int64_t) const { return {}; }
+  __device__ void operator()(int64_t row, int64_t col, float x, float, Col) const {
+    if (c_dtype == FOCUS_BF16)
+      reinterpret_cast<__bf16*>(c)[row * ldc + col] = (__bf16)(x * alpha);
+    else
+      reinterpret_cast<float*>(c)[row * ldc + col] = x * alpha;
+  }
+};
+
+// The layer's Q/K/V projection: columns [Q heads | K heads | V heads]; RoPE on
+// Q and K at the token's position in its augmented stream (the summary tokens
+// hold real positions), interleaved pairs (2i, 2i + 1) rotated by
+// pos * theta^(-2i/D): the angle is formed in float64 in revolutions
+// (pos * theta^(-2i/D) / 2 pi), reduced to [0, 1), and fed to the hardware
+// sine / cosine, which take revolutions.  K and V rows of summary tokens also
+// go straight to their cache row (the compaction pass, fused into the store).
+struct QkvEpi {
+  static constexpr bool kPair = true;
+  struct Col {
+    int seg;          // 0 Q, 1 K, 2 V
+    int64_t c;        // column inside its tensor row
+    double rev;       // revolutions per position of this column's pair (0: no rotation)
+    bool odd;
+  };
+  int32_t H, Hkv, D, batch;
+  double log2_theta;   // <= 0: no rotation
+  void* q;
+  void* k;
+  void* v;
+  const int32_t* tok_pos;
+  const uint8_t* tok_kind;
+  const int32_t* tok_kmer;
+  const int32_t* tok_win;
+  const int32_t* win_seq;
+  int64_t tok_base;
+  void* cache_k;
+  void* cache_v;
+  int64_t cache_cap;
+  int32_t* cache_len;
+  int32_t* err;
+  __device__ Col col(int64_t col) const {
+    const int64_t qc = (int64_t)H * D, kc = (int64_t)Hkv * D;
+    Col r;
+    r.seg = col < qc ? 0 : col < qc + kc ? 1 : 2;
+    r.c = r.seg == 0 ? col : r.seg == 1 ? col - qc : col - qc - kc;
+    const int dd = (int)(r.c % D);
+    r.odd = dd & 1;
+    r.rev = (r.seg < 2 && log2_theta > 0.0) ? exp2(-(2.0 * (dd >> 1) / D) * log2_theta) * 0.15915494309189533577 : 0.0;
+    return r;
+  }
+  __device__ void operator()(int64_t row, int64_t, float x, float xp, const Col& cl) const {
+    const int64_t t = tok_base + row;
+    const int64_t qc = (int64_t)H * D, kc = (int64_t)Hkv * D;
+    const int seg = cl.seg;
+    const int64_t c = cl.c;
+    float y = x;
+    if (cl.rev > 0.0) {
+      const double a = (double)tok_pos[t] * cl.rev;
+      const float r = (float)(a - floor(a));           // revolutions in [0, 1)
+      const float sn = __builtin_amdgcn_sinf(r), cs = __builtin_amdgcn_cosf(r);
+      // (e, o) -> (e cos - o sin, e sin + o cos); the partner holds the other half
+      y = cl.odd ? fmaf(xp, sn, x * cs) : fmaf(-xp, sn, x * cs);
+    }
+    const __bf16 yb = (__bf16)y;
+    __bf16* dst = reinterpret_cast<__bf16*>(seg == 0 ? q : seg == 1 ? k : v);
+    dst[row * (seg == 0 ? qc : kc) + c] = yb;
+    if (seg > 0 && cache_k && tok_kind[t] == FOCUS_TOK_SUMMARY) {
+      const int32_t cr = tok_kmer[t];
+      const int32_t b = win_seq[tok_win[t]];
+      if (cr < 0 || cr >= cache_cap || b < 0 || b >= batch) {
+        focus::raise_err(err, FOCUS_ERR_CAPACITY);
+        return;
+      }
+      __bf16* cdst = reinterpret_cast<__bf16*>(seg == 1 ? cache_k : cache_v);
+      cdst[((int64_t)b * cache_cap + cr) * kc + c] = yb;
+      if (seg == 1 && c == 0 && cache_len) atomicMax(cache_len + b, cr + 1);
+    }
+  }
+};
+
+template <class Epi>
+__global__ __launch_bounds__(kThreads, 2) void gemm_bf16(focus_gemm_desc d, int64_t m_tiles, Epi epi) {
   __shared__ __attribute__((aligned(1024))) char abuf0[kATile], abuf1[kATile];
   __shared__ __attribute__((aligned(1024))) char bbuf0[kBTile], bbuf1[kBTile];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, l32 = lane & 31, g = lane >> 5;
@@ -130,23 +223,22 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16(focus_gemm_desc d, int6
     __syncthreads();
   }
 
-  // acc[i][j][v] = C[m0 + wm + 32 i + 8 (v / 4) + 4 g + v % 4][n0 + wn + 32 j + l32]
+  // acc[i][j][v] = C[m0 + wm + 32 i + 8 (v / 4) + 4 g + v % 4][n0 + wn + 32 j + l32];
+  // column col ^ 1 sits in lane ^ 1 (DPP quad swap, taken before any branch)
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int j = 0; j < 2; ++j) {
+    const int64_t col = n0 + wn + 32 * j + l32;
+    const typename Epi::Col cl = epi.col(col);
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int64_t row = m0 + wm + 32 * i + 8 * (v >> 2) + 4 * g + (v & 3);
-      if (row >= d.m) continue;
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int64_t col = n0 + wn + 32 * j + l32;
-        const float x = acc[i][j][v] * d.alpha;
-        if (d.c_dtype == FOCUS_BF16)
-          reinterpret_cast<__bf16*>(d.c)[row * d.ldc + col] = (__bf16)x;
-        else
-          reinterpret_cast<float*>(d.c)[row * d.ldc + col] = x;
+      for (int v = 0; v < 16; ++v) {
+        const int64_t row = m0 + wm + 32 * i + 8 * (v >> 2) + 4 * g + (v & 3);
+        const float x = acc[i][j][v];
+        const float xp = Epi::kPair ? focus::dpp_xor1(x) : 0.f;
+        if (row < d.m) epi(row, col, x, xp, cl);
       }
-    }
+  }
 }
 
 }  // namespace
@@ -165,7 +257,63 @@ extern "C" focus_status focus_gemm(const focus_gemm_desc* d, focus_stream_t stre
     return FOCUS_E_ARG;
   const int64_t m_tiles = focus::ceil_div(d->m, kBM), n_tiles = d->n / kBN;
   if (m_tiles * n_tiles > INT32_MAX) return FOCUS_E_SHAPE;
-  hipLaunchKernelGGL(gemm_bf16, dim3((uint32_t)(m_tiles * n_tiles)), dim3(kThreads), 0,
-                     reinterpret_cast<hipStream_t>(stream), *d, m_tiles);
+  const PlainEpi epi = {d->c, d->ldc, d->c_dtype, d->alpha};
+  hipLaunchKernelGGL(gemm_bf16<PlainEpi>, dim3((uint32_t)(m_tiles * n_tiles)), dim3(kThreads), 0,
+                     reinterpret_cast<hipStream_t>(stream), *d, m_tiles, epi);
+  return focus::launch_status();
+}
+
+extern "C" focus_status focus_qkv_project(const focus_qkv_desc* q, focus_stream_t stream) {
+  if (!q) return FOCUS_E_NULL;
+  if (q->dtype != FOCUS_BF16) return q->dtype == FOCUS_F32 ? FOCUS_E_UNSUPPORTED : FOCUS_E_DTYPE;
+  if (q->n_heads <= 0 || q->n_kv_heads <= 0 || q->d_model <= 0 || q->batch < 0 || q->n_rows < 0 ||
+      q->tok_base < 0 || !(q->rope_theta == q->rope_theta) || (q->rope_theta > 0.f && q->rope_theta <= 1.f))
+    return FOCUS_E_ARG;
+  if (q->head_dim != 64 && q->head_dim != 128) return FOCUS_E_UNSUPPORTED;
+  if (q->n_heads % q->n_kv_heads) return FOCUS_E_SHAPE;
+  const int64_t n = ((int64_t)q->n_heads + 2 * q->n_kv_heads) * q->head_dim;
+  if (n % kBN || q->d_model % kBKk) return FOCUS_E_UNSUPPORTED;
+  if (q->tok_base + q->n_rows > q->totals.n_tokens) return FOCUS_E_SHAPE;
+  if (q->n_rows == 0) return FOCUS_OK;
+  if (!q->hidden || !q->w_qkv || !q->q || !q->k || !q->v || !q->tok_pos) return FOCUS_E_NULL;
+  if (q->cache_k && (!q->cache_v || !q->tok_kind || !q->tok_kmer || !q->tok_win || !q->win_seq))
+    return FOCUS_E_NULL;
+  if (q->cache_k && q->cache_cap < q->totals.max_cache_per_seq && q->tok_base == 0 && q->n_rows == q->totals.n_tokens)
+    return FOCUS_E_CAPACITY;
+  if (!focus::aligned16(q->hidden) || !focus::aligned16(q->w_qkv)) return FOCUS_E_ARG;
+  focus_gemm_desc g = {};
+  g.m = q->n_rows;
+  g.n = n;
+  g.k = q->d_model;
+  g.a = q->hidden;
+  g.lda = q->d_model;
+  g.a_nrows = q->n_rows;
+  g.b = q->w_qkv;
+  g.ldb = n;
+  g.err = q->err;
+  QkvEpi e;
+  e.H = q->n_heads;
+  e.Hkv = q->n_kv_heads;
+  e.D = q->head_dim;
+  e.batch = q->batch;
+  e.log2_theta = q->rope_theta > 0.f ? log2((double)q->rope_theta) : 0.0;
+  e.q = q->q;
+  e.k = q->k;
+  e.v = q->v;
+  e.tok_pos = q->tok_pos;
+  e.tok_kind = q->tok_kind;
+  e.tok_kmer = q->tok_kmer;
+  e.tok_win = q->tok_win;
+  e.win_seq = q->win_seq;
+  e.tok_base = q->tok_base;
+  e.cache_k = q->cache_k;
+  e.cache_v = q->cache_v;
+  e.cache_cap = q->cache_cap;
+  e.cache_len = q->cache_len;
+  e.err = q->err;
+  const int64_t m_tiles = focus::ceil_div(g.m, kBM), n_tiles = n / kBN;
+  if (m_tiles * n_tiles > INT32_MAX) return FOCUS_E_SHAPE;
+  hipLaunchKernelGGL(gemm_bf16<QkvEpi>, dim3((uint32_t)(m_tiles * n_tiles)), dim3(kThreads), 0,
+                     reinterpret_cast<hipStream_t>(stream), g, m_tiles, e);
   return focus::launch_status();
 }
