@@ -68,18 +68,31 @@ struct Item {
 };
 
 // Block -> (listed window, head, query tile).  Blocks go round robin over the
-// XCDs; the QT query tiles of pair p = list_idx * H + h all get blocks on XCD
-// p % 8, consecutive in that XCD's dispatch order, and pairs are dispatched in
-// increasing p.
+// XCDs, and the QT query tiles of a (window, head) pair get consecutive blocks
+// of one XCD (they share its K/V tiles through that XCD's L2).  When H is a
+// multiple of the XCD count, XCD x owns heads x, x + 8, ... and walks them one
+// at a time, each over all listed windows in list order: the workgroups that
+// run together on an XCD then stream the same cache rows of one head at about
+// the same time, so each row is fetched into its L2 once for all of them.
+// Otherwise pair p = list_idx * H + h goes to XCD p % 8, in increasing p.
 __device__ inline Item map_block(int64_t bid, int64_t n_pairs, int H, int QT) {
   const int x = (int)(bid % focus::kXcds);
   const int64_t s = bid / focus::kXcds;
   Item it;
   it.qt = (int)(s % QT);
-  const int64_t p = (s / QT) * focus::kXcds + x;
-  it.valid = p < n_pairs;
-  it.list_idx = p / H;
-  it.h = (int)(p % H);
+  const int64_t j = s / QT;  // this XCD's j-th pair
+  if (H % focus::kXcds == 0) {
+    const int64_t nwl = n_pairs / H;  // listed windows
+    const int64_t hl = nwl > 0 ? j / nwl : 0;
+    it.valid = nwl > 0 && hl < H / focus::kXcds;
+    it.list_idx = nwl > 0 ? j % nwl : 0;
+    it.h = (int)(hl * focus::kXcds + x);
+  } else {
+    const int64_t p = j * focus::kXcds + x;
+    it.valid = p < n_pairs;
+    it.list_idx = p / H;
+    it.h = (int)(p % H);
+  }
   return it;
 }
 
@@ -139,8 +152,14 @@ __global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_d
   // Two K and two V tile buffers as separate arrays, referenced statically by
   // a loop unrolled by two: the compiler can then tell a tile being read from
   // the one being filled, and waits for the copies only at the barrier.
+  // Under C(t) a third K and V buffer lets copies run two steps ahead (one
+  // workgroup per CU: the register budget allows no second, so the LDS is
+  // there); the k-mer-local and summary-query modes keep two.
+  constexpr int kStages = (!KL && !SQ) ? 3 : 2;
   __shared__ __attribute__((aligned(1024))) char kbuf0[C::kTile], kbuf1[C::kTile];
   __shared__ __attribute__((aligned(1024))) char vbuf0[C::kTile], vbuf1[C::kTile];
+  __shared__ __attribute__((aligned(1024))) char kbuf2[kStages == 3 ? C::kTile : 16];
+  __shared__ __attribute__((aligned(1024))) char vbuf2[kStages == 3 ? C::kTile : 16];
 
   const int tid = threadIdx.x;
   const Item it = map_block(blockIdx.x, n_pairs, d.n_heads, QT);
@@ -319,17 +338,27 @@ __global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_d
     const int lim = KL ? (in_cache ? jq - row0 : qi - row0) : (in_cache ? Cw - row0 - 1 : qi - row0);
     const int lo = KL ? (in_cache ? (Cw > 0 ? 0 : 1) - row0 : qlo - row0) : 0;
     if (live) {
+      // S^T = K Q^T: the two 32-key blocks as two independent MFMA chains,
+      // each K operand read one k-step ahead of its MFMA.
       f32x16 sacc[2];
 #pragma unroll
-      for (int st = 0; st < 2; ++st) {
+      for (int st = 0; st < 2; ++st)
 #pragma unroll
         for (int v = 0; v < 16; ++v) sacc[st][v] = 0.f;
-        const int r = st * 32 + l32;
+      bf16x8 ka[2], kn[2];
 #pragma unroll
-        for (int s = 0; s < C::kKsteps; ++s) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(kl + k_off<D>(r, 2 * s + g));
-          sacc[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[s], sacc[st], 0, 0, 0);
+      for (int st = 0; st < 2; ++st) ka[st] = *reinterpret_cast<const bf16x8*>(kl + k_off<D>(st * 32 + l32, g));
+#pragma unroll
+      for (int s = 0; s < C::kKsteps; ++s) {
+        if (s + 1 < C::kKsteps) {
+#pragma unroll
+          for (int st = 0; st < 2; ++st)
+            kn[st] = *reinterpret_cast<const bf16x8*>(kl + k_off<D>(st * 32 + l32, 2 * (s + 1) + g));
         }
+#pragma unroll
+        for (int st = 0; st < 2; ++st) sacc[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[st], qf[s], sacc[st], 0, 0, 0);
+#pragma unroll
+        for (int st = 0; st < 2; ++st) ka[st] = kn[st];
       }
       // sacc[st][v] = score of query qi with tile key 32 st + 8 (v/4) + 4 g + v%4
       if (need_mask) {
@@ -347,7 +376,10 @@ __global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_d
       for (int st = 0; st < 2; ++st)
 #pragma unroll
         for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[st][v]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      {
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+        mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));  // with lane ^ 32
+      }
       const float m_new = fmaxf(m_run, mx * sc);
       if (__any(m_new - m_run > kLazy)) {
         const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
@@ -392,17 +424,51 @@ __global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_d
     }
   };
 
-  // The barrier closing each step also waits for the next tile's copies.
-  issue_tile(0, kbuf0, vbuf0);
-  __syncthreads();
-  for (int t = 0; t < ntiles; t += 2) {
-    if (t + 1 < ntiles) issue_tile(t + 1, kbuf1, vbuf1);
-    compute_tile(t, kbuf0, vbuf0);
+  if constexpr (kStages == 2) {
+    // The barrier closing each step also waits for the next tile's copies.
+    issue_tile(0, kbuf0, vbuf0);
     __syncthreads();
-    if (t + 1 >= ntiles) break;
-    if (t + 2 < ntiles) issue_tile(t + 2, kbuf0, vbuf0);
-    compute_tile(t + 1, kbuf1, vbuf1);
-    __syncthreads();
+    for (int t = 0; t < ntiles; t += 2) {
+      if (t + 1 < ntiles) issue_tile(t + 1, kbuf1, vbuf1);
+      compute_tile(t, kbuf0, vbuf0);
+      __syncthreads();
+      if (t + 1 >= ntiles) break;
+      if (t + 2 < ntiles) issue_tile(t + 2, kbuf0, vbuf0);
+      compute_tile(t + 1, kbuf1, vbuf1);
+      __syncthreads();
+    }
+  } else {
+    // Tile t lives in buffers t % 3.  Step t first starts the copies of tile
+    // t + 2 (into the buffers tile t - 1 left; past the last tile it copies
+    // the last tile again, into a buffer no later step reads), and ends by
+    // waiting until only those copies are in flight (tile t + 1 has landed),
+    // then a barrier: a copy has two steps to land.  The signal fences keep
+    // the compiler from moving memory accesses across the wait and barrier.
+    auto end_step = [&]() {
+      constexpr int kVm = 2 * kDma;  // s_waitcnt vmcnt(kVm) expcnt(7) lgkmcnt(0)
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
+      __builtin_amdgcn_s_waitcnt((kVm & 15) | ((kVm >> 4) << 14) | (7 << 4) | (0 << 8));
+      __builtin_amdgcn_s_barrier();
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    };
+    issue_tile(0, kbuf0, vbuf0);
+    issue_tile(min(1, ntiles - 1), kbuf1, vbuf1);
+    __syncthreads();  // tiles 0 and 1 have landed (a full wait: the compiler
+                      // then knows no copy is pending when the loop starts)
+    for (int t = 0; t < ntiles; t += 3) {
+      issue_tile(min(t + 2, ntiles - 1), kbuf2, vbuf2);
+      compute_tile(t, kbuf0, vbuf0);
+      end_step();
+      if (t + 1 >= ntiles) break;
+      issue_tile(min(t + 3, ntiles - 1), kbuf0, vbuf0);
+      compute_tile(t + 1, kbuf1, vbuf1);
+      end_step();
+      if (t + 2 >= ntiles) break;
+      issue_tile(min(t + 4, ntiles - 1), kbuf1, vbuf1);
+      compute_tile(t + 2, kbuf2, vbuf2);
+      end_step();
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // no copy into LDS outlives the block
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
