@@ -242,22 +242,29 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16(focus_gemm_desc d, int6
 }
 
 
-// Large products (N a multiple of 256, M >= 256): one workgroup = 4 waves = a
-// 256 x 256 tile of C, each wave 128 x 128 as 4 x 4 blocks of
-// v_mfma_f32_32x32x16_bf16.  Per 16-deep k-step a wave reads 4 A and 4 B
-// operands from LDS for 16 MFMAs, half the LDS traffic per MFMA of the
+// Large products (N a multiple of 256, M >= 256, K a multiple of 128): one
+// workgroup = 4 waves = a 256 x 256 tile of C, each wave 128 x 128 as 4 x 4
+// blocks of v_mfma_f32_32x32x16_bf16.  Per 16-deep k-step a wave reads 4 A and
+// 4 B operands from LDS for 16 MFMAs, half the LDS traffic per MFMA of the
 // 128 x 128 tile (whose 64 x 64 waves read 2 + 2 for 4); one wave per SIMD
-// (the 256 accumulators fill the AGPRs).  Same copy scheme and swizzles, B
-// rows now 512 bytes (eight 64-byte granules, XOR-swizzled by row as above).
-constexpr int kBM2 = 256, kBN2 = 256;
+// (the 256 accumulators fill the AGPRs).  K advances 32 at a time through four
+// LDS stages (A 256 x 64 B + B 32 x 512 B = 32 KB each): the copies of step
+// t + 3 start in step t, so a copy has three steps to land, and a step ends on
+// a partial wait (only the two younger steps' copies in flight) plus a barrier.
+// A rows are 64 bytes: 16-byte chunk c of row r sits at c ^ ((r / 4) mod 4), so
+// the 8 rows one quarter-wave reads fall into distinct bank groups; B rows are
+// 512 bytes, 64-byte granules XOR-swizzled by (row mod 4) as above.
+constexpr int kBM2 = 256, kBN2 = 256, kBK2 = 32;
+constexpr int kARow2 = kBK2 * 2;                 // bytes per A tile row (64)
 constexpr int kBRow2 = kBN2 * 2;                 // bytes per B tile row (512)
-constexpr int kATile2 = kBM2 * kARow;            // 32 KB
-constexpr int kBTile2 = kBKk * kBRow2;           // 32 KB
+constexpr int kATile2 = kBM2 * kARow2;           // 16 KB
+constexpr int kBTile2 = kBK2 * kBRow2;           // 16 KB
+constexpr int kStage2 = kATile2 + kBTile2;       // A then B
 
 template <class Epi>
 __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_wide(focus_gemm_desc d, int64_t m_tiles, Epi epi) {
-  __shared__ __attribute__((aligned(1024))) char abuf0[kATile2], abuf1[kATile2];
-  __shared__ __attribute__((aligned(1024))) char bbuf0[kBTile2], bbuf1[kBTile2];
+  // One array per stage: the compiler tracks the copies in flight per array.
+  __shared__ __attribute__((aligned(1024))) char st0[kStage2], st1[kStage2], st2[kStage2], st3[kStage2];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, l32 = lane & 31, g = lane >> 5;
   const int64_t n_tiles = d.n / kBN2, per_group = (int64_t)kGroupM * n_tiles;
   const int64_t grp0 = blockIdx.x / per_group, in_grp = blockIdx.x % per_group;
@@ -266,38 +273,41 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_wide(focus_gemm_desc d,
   const int64_t m0 = mt * kBM2, n0 = nt * kBN2;
   const int wm = (wave & 1) * 128, wn = (wave >> 1) * 128;  // this wave's 128 x 128 in the tile
 
-  // Copy plan: A tile = 32 wave-loads of 1 KB (8 rows x 128 B), 8 per wave;
-  // B tile = 32 wave-loads (2 rows x 512 B), 8 per wave.
+  // Copy plan: A tile = 16 wave-loads of 1 KB (16 rows x 64 B), 4 per wave;
+  // B tile = 16 wave-loads (2 rows x 512 B), 4 per wave.  Lane p of a row
+  // fetches the global chunk the swizzled layout keeps at its slot.
   const char* A = reinterpret_cast<const char*>(d.a);
   const char* B = reinterpret_cast<const char*>(d.b);
   const int64_t a_ld = d.lda * 2, b_ld = d.ldb * 2;
-  const char* a_src[8];
+  const char* a_src[4];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int r = (wave * 8 + i) * 8 + (lane >> 3), p = lane & 7;   // A tile row, 16-B slot
+  for (int i = 0; i < 4; ++i) {
+    const int r = (wave * 4 + i) * 16 + (lane >> 2), p = lane & 3;  // A tile row, 16-B slot
     const int64_t gm = min(m0 + r, d.m - 1);                         // ragged M: repeat the last row
     int64_t ar = d.a_rows ? d.a_rows[gm] : gm;
     if (ar < 0 || ar >= d.a_nrows) {
       focus::raise_err(d.err, FOCUS_ERR_BOUNDS);
       ar = 0;
     }
-    a_src[i] = A + ar * a_ld + ((p ^ (r & 7)) << 4);
+    a_src[i] = A + ar * a_ld + ((p ^ ((r >> 2) & 3)) << 4);
   }
-  // B tile row of wave-load i: (wave * 8 + i) * 2 + lane / 32; slot lane % 32
+  // B tile row of wave-load i: (wave * 4 + i) * 2 + lane / 32 (row mod 4
+  // alternates with i); slot lane % 32
   const int pb = lane & 31;
-  const int brow0 = wave * 16 + (lane >> 5);
-  const uint32_t b_col = (uint32_t)((((pb >> 2) ^ (brow0 & 3)) * 4 + (pb & 3)) * 16);  // brow & 3 = brow0 & 3 for even steps
+  const int brow0 = wave * 8 + (lane >> 5);
+  const uint32_t b_col0 = (uint32_t)((((pb >> 2) ^ (brow0 & 3)) * 4 + (pb & 3)) * 16);
   const uint32_t b_col1 = (uint32_t)((((pb >> 2) ^ ((brow0 + 2) & 3)) * 4 + (pb & 3)) * 16);
+  const char* b_src = B + (int64_t)brow0 * b_ld + n0 * 2;
 
-  auto issue = [&](int64_t k0, char* ab, char* bb) {
+  // wave copy pair i (A rows and B rows) of the step at k0 into a stage
+  auto issue_pair = [&](int64_t k0, char* stage, int i) {
+    __builtin_amdgcn_global_load_lds(a_src[i] + k0 * 2, (lds_void*)(stage + (wave * 4 + i) * 1024), 16, 0, 0);
+    const char* gb = b_src + (k0 + 2 * i) * b_ld + ((i & 1) ? b_col1 : b_col0);
+    __builtin_amdgcn_global_load_lds(gb, (lds_void*)(stage + kATile2 + (wave * 4 + i) * 1024), 16, 0, 0);
+  };
+  auto issue = [&](int64_t k0, char* stage) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const char* ga = a_src[i] + k0 * 2;
-      __builtin_amdgcn_global_load_lds(ga, (lds_void*)(ab + (wave * 8 + i) * 1024), 16, 0, 0);
-      const int brow = brow0 + 2 * i;
-      const char* gb = B + (k0 + brow) * b_ld + n0 * 2 + ((i & 1) ? b_col1 : b_col);
-      __builtin_amdgcn_global_load_lds(gb, (lds_void*)(bb + (wave * 8 + i) * 1024), 16, 0, 0);
-    }
+    for (int i = 0; i < 4; ++i) issue_pair(k0, stage, i);
   };
 
   f32x16 acc[4][4];
@@ -308,95 +318,121 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_wide(focus_gemm_desc d,
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  auto compute = [&](const char* ab, const char* bb) {
+  // Computes the step in `stage` and starts the copies of the step at k_nxt
+  // into `nxt`, one pair after every 8 MFMAs: a wave that sends all its
+  // copies at once stalls until the address unit has taken them.
+  auto compute = [&](const char* stage, int64_t k_nxt, char* nxt) {
     // Per-lane LDS offsets, rebuilt each step behind an empty asm statement
-    // (not hoisted per buffer; one offset from each buffer, so the compiler
-    // can tell the buffer being read from the one being filled).
-    //   A: row wm + 32 i + l32, chunk 2 s + g at (2 s + g) ^ (l32 & 7)
+    // (not hoisted per stage; one offset from each stage, so the compiler can
+    // tell the stage being read from the ones being filled).
+    //   A: row wm + 32 i + l32, chunk 2 s + g at (2 s + g) ^ ((l32 / 4) mod 4)
     //   B: transposing read of rows 16 s + 8 (grp / 2) + ri (+ 4), byte
     //      2 (wn + 32 j + 16 (grp & 1) + 4 bq), granule ((wn / 32 + j) ^ ri)
     const int grp = lane >> 4, ri = (lane >> 2) & 3, bq = lane & 3;
-    int ao[4], bo[4];
+    int ao[2], bo[4];
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      ao[s] = (wm + l32) * kARow + (((2 * s + g) ^ (l32 & 7)) << 4);
+    for (int s = 0; s < 2; ++s) {
+      ao[s] = (wm + l32) * kARow2 + (((2 * s + g) ^ ((l32 >> 2) & 3)) << 4);
       asm volatile("" : "+v"(ao[s]));
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      bo[j] = (8 * (grp >> 1) + ri) * kBRow2 + ((((wn >> 5) + j) ^ ri) << 6) + 32 * (grp & 1) + 8 * bq;
+      bo[j] = kATile2 + (8 * (grp >> 1) + ri) * kBRow2 + ((((wn >> 5) + j) ^ ri) << 6) + 32 * (grp & 1) + 8 * bq;
       asm volatile("" : "+v"(bo[j]));
     }
-    // Operands of k-step s + 1 are read while the 16 MFMAs of k-step s run
-    // (two register sets; the scheduling barriers keep the compiler from
-    // hoisting every read of the tile up front).
+    // Operands of k-step s + 1 are read while the 16 MFMAs of k-step s run.
     bf16x8 af[2][4], bf[2][4];
     auto load = [&](int s, int buf) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) af[buf][i] = *reinterpret_cast<const bf16x8*>(ab + (ao[s] + 32 * i * kARow));
+      for (int i = 0; i < 4; ++i) af[buf][i] = *reinterpret_cast<const bf16x8*>(stage + (ao[s] + 32 * i * kARow2));
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(bb + (bo[j] + 16 * s * kBRow2)));
-        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(bb + (bo[j] + (16 * s + 4) * kBRow2)));
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(stage + (bo[j] + 16 * s * kBRow2)));
+        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(stage + (bo[j] + (16 * s + 4) * kBRow2)));
         bf[buf][j] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
       }
     };
     load(0, 0);
+    load(1, 1);
 #pragma unroll
-    for (int s = 0; s < kBKk / 16; ++s) {
-      if (s + 1 < kBKk / 16) load(s + 1, (s + 1) & 1);
+    for (int s = 0; s < 2; ++s) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < 4; ++i) {
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s & 1][i], bf[s & 1][j], acc[i][j], 0, 0, 0);
-      __builtin_amdgcn_sched_barrier(0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s][i], bf[s][j], acc[i][j], 0, 0, 0);
+        if (i & 1) {
+          __builtin_amdgcn_sched_barrier(0);
+          issue_pair(k_nxt, nxt, 2 * s + (i >> 1));
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
     }
   };
 
-  // Pairs of k-steps (buffers 0, 1), then an odd last step in buffer 0.
-  const int64_t nk = d.k / kBKk;
-  issue(0, abuf0, bbuf0);
+  // Step t: start the copies of step t + 3 (past the end, of the last step
+  // again: every step starts the same number, and that stage is not read
+  // again), compute step t, wait until step t + 1 has landed, barrier.
+  const int64_t nk = d.k / kBK2;
+  auto end_step = [&]() {
+    constexpr int kVm = 2 * 8;  // two younger steps of 8 wave copies: vmcnt(16) expcnt(7) lgkmcnt(0)
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt((kVm & 15) | ((kVm >> 4) << 14) | (7 << 4) | (0 << 8));
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  };
+  auto step = [&](int64_t t, const char* cur, char* nxt) {
+    compute(cur, min(t + 3, nk - 1) * kBK2, nxt);
+    end_step();
+  };
+  issue(0, st0);
+  issue(min((int64_t)1, nk - 1) * kBK2, st1);
+  issue(min((int64_t)2, nk - 1) * kBK2, st2);
   __syncthreads();
-  for (int64_t t = 0; t + 1 < nk; t += 2) {
-    issue((t + 1) * kBKk, abuf1, bbuf1);
-    compute(abuf0, bbuf0);
-    __syncthreads();
-    if (t + 2 < nk) issue((t + 2) * kBKk, abuf0, bbuf0);
-    compute(abuf1, bbuf1);
-    __syncthreads();
+  // nk is a multiple of 4 (a partial round would need exits inside the
+  // loop, around which the compiler moves the accumulators out of the AGPRs)
+  for (int64_t t = 0; t < nk; t += 4) {
+    step(t, st0, st3);
+    step(t + 1, st1, st0);
+    step(t + 2, st2, st1);
+    step(t + 3, st3, st2);
   }
-  if (nk & 1) compute(abuf0, bbuf0);
+  __builtin_amdgcn_s_waitcnt(0);  // no copy into LDS outlives the block
+  __syncthreads();                // and no wave still reads a stage
 
-  // acc[i][j][v] = C[m0 + wm + 32 i + 8 (v / 4) + 4 g + v % 4][n0 + wn + 32 j + l32].
-  // The column data is derived from a copy of the lane id taken here, so that
-  // none of it is computed before (and kept live through) the k loop.
-  int lc = l32;
-  asm volatile("" : "+v"(lc));
-  // Row-major order (row block i, row v, then the four column blocks), so a
-  // row's per-token data is fetched once for its four columns.
-  typename Epi::Col cl[4];
+  // Epilogue through LDS: each wave parks 64 x 128 of its float32 results
+  // (half its tile) in one stage, then walks them a row at a time, a lane
+  // taking two adjacent columns (a RoPE pair): the epilogue code appears once
+  // and every store of a row is contiguous.  Same-wave LDS accesses complete
+  // in order, so no barrier is needed between the writes and the reads.
+  //   acc[i][j][v] = C[m0 + wm + 32 i + 8 (v / 4) + 4 g + v % 4][n0 + wn + 32 j + l32]
+  float* ct = reinterpret_cast<float*>(wave == 0 ? st0 : wave == 1 ? st1 : wave == 2 ? st2 : st3);
+  const int64_t c0 = n0 + wn + 2 * lane;
+  const typename Epi::Col cl0 = epi.col(c0), cl1 = epi.col(c0 + 1);
 #pragma unroll
-  for (int j = 0; j < 4; ++j) cl[j] = epi.col(n0 + wn + 32 * j + lc);
+  for (int h = 0; h < 2; ++h) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+    for (int i2 = 0; i2 < 2; ++i2)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int64_t row = m0 + wm + 32 * i + 8 * (v >> 2) + 4 * g + (v & 3);
+      for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float x = acc[i][j][v];
-        const float xp = Epi::kPair ? focus::dpp_xor1(x) : 0.f;
-        if (row < d.m) epi(row, n0 + wn + 32 * j + lc, x, xp, cl[j]);
-      }
+        for (int v = 0; v < 16; ++v)
+          ct[(32 * i2 + 8 * (v >> 2) + 4 * g + (v & 3)) * 128 + 32 * j + l32] = acc[2 * h + i2][j][v];
+    const int64_t rows = min((int64_t)64, d.m - (m0 + wm + 64 * h));
+    for (int r = 0; r < rows; ++r) {
+      const float2 x = reinterpret_cast<const float2*>(ct)[r * 64 + lane];
+      const int64_t row = m0 + wm + 64 * h + r;
+      epi(row, c0, x.x, x.y, cl0);
+      epi(row, c0 + 1, x.y, x.x, cl1);
     }
+  }
 }
 
 // Launch C = A B (+ epilogue) with the wide tile where N and M allow.
 template <class Epi>
 focus_status launch_gemm(const focus_gemm_desc& d, const Epi& epi, focus_stream_t stream) {
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  if (d.n % kBN2 == 0 && d.m >= kBM2) {
+  if (d.n % kBN2 == 0 && d.m >= kBM2 && d.k % (4 * kBK2) == 0) {
     const int64_t m_tiles = focus::ceil_div(d.m, kBM2), n_tiles = d.n / kBN2;
     if (m_tiles * n_tiles > INT32_MAX) return FOCUS_E_SHAPE;
     hipLaunchKernelGGL(gemm_bf16_wide<Epi>, dim3((uint32_t)(m_tiles * n_tiles)), dim3(kThreads), 0, s, d, m_tiles, epi);
