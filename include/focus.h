@@ -528,7 +528,8 @@ focus_status focus_gemm(const focus_gemm_desc* d, focus_stream_t stream);
  * V heads; q [n_rows, H, D], k / v [n_rows, H_kv, D]; all bf16 (float32
  * accumulation and rotation, then rounding).  rope_theta <= 0 skips the
  * rotation.  cache_k NULL skips the cache write.  Requirements: (H + 2 H_kv) D
- * a multiple of 128, d_model a multiple of 64.  Errors: E_NULL, E_ARG, E_DTYPE,
+ * a multiple of 128, d_model a multiple of 64, hidden and w_qkv 16-byte
+ * aligned, q, k, v and the caches 4-byte aligned.  Errors: E_NULL, E_ARG, E_DTYPE,
  * E_SHAPE, E_UNSUPPORTED (f32, tile multiples), E_CAPACITY (whole layout and
  * cache_cap < max_cache_per_seq), E_HIP; a cache row outside the cache is
  * skipped with FOCUS_ERR_CAPACITY. */

@@ -53,22 +53,36 @@ struct PlainEpi {
     else
       reinterpret_cast<float*>(c)[row * ldc + col] = x * alpha;
   }
+  // columns col (even) and col + 1 of a row
+  __device__ void pair(int64_t row, int64_t col, float x0, float x1, Col) const {
+    const int64_t i = row * ldc + col;
+    if (c_dtype == FOCUS_BF16 && !(i & 1)) {
+      reinterpret_cast<uint32_t*>(c)[i >> 1] = focus::pack_bf16x2(x0 * alpha, x1 * alpha);
+    } else {
+      (*this)(row, col, x0, x1, Col{});
+      (*this)(row, col + 1, x1, x0, Col{});
+    }
+  }
 };
 
 // The layer's Q/K/V projection: columns [Q heads | K heads | V heads]; RoPE on
 // Q and K at the token's position in its augmented stream (the summary tokens
 // hold real positions), interleaved pairs (2i, 2i + 1) rotated by
-// pos * theta^(-2i/D): the angle is formed in float64 in revolutions
-// (pos * theta^(-2i/D) / 2 pi), reduced to [0, 1), and fed to the hardware
-// sine / cosine, which take revolutions.  K and V rows of summary tokens also
-// go straight to their cache row (the compaction pass, fused into the store).
+// pos * theta^(-2i/D).  The angle is taken in revolutions,
+// pos * theta^(-2i/D) / 2 pi, whose fraction is what the hardware sine and
+// cosine need: the per-pair rate is held as a 64-bit binary fraction (from its
+// float64 value), so the fraction of pos * rate is the top 32 bits of a
+// 32 x 64-bit integer product (two 32-bit multiplies) — exact to 2^-32 of a
+// revolution for any position.  K and V rows of summary tokens also go
+// straight to their cache row (the compaction pass, fused into the store).
 struct QkvEpi {
   static constexpr bool kPair = true;
   struct Col {
     int seg;          // 0 Q, 1 K, 2 V
     int64_t c;        // column inside its tensor row
-    double rev;       // revolutions per position of this column's pair (0: no rotation)
+    bool rot;         // rotated (a Q or K column, theta given)
     bool odd;
+    uint32_t r_hi, r_lo;  // revolutions per position of the pair, as a 64-bit fraction
   };
   int32_t H, Hkv, D, batch;
   double log2_theta;   // <= 0: no rotation
@@ -93,8 +107,18 @@ struct QkvEpi {
     r.c = r.seg == 0 ? col : r.seg == 1 ? col - qc : col - qc - kc;
     const int dd = (int)(r.c % D);
     r.odd = dd & 1;
-    r.rev = (r.seg < 2 && log2_theta > 0.0) ? exp2(-(2.0 * (dd >> 1) / D) * log2_theta) * 0.15915494309189533577 : 0.0;
+    r.rot = r.seg < 2 && log2_theta > 0.0;
+    const double rev = r.rot ? exp2(-(2.0 * (dd >> 1) / D) * log2_theta) * 0.15915494309189533577 : 0.0;
+    const double hi = floor(rev * 4294967296.0);
+    r.r_hi = (uint32_t)hi;
+    r.r_lo = (uint32_t)((rev * 4294967296.0 - hi) * 4294967296.0);
     return r;
+  }
+  // fraction of tok_pos[t] * rate, in revolutions, [0, 1]
+  __device__ float turn(int64_t t, const Col& cl) const {
+    const uint32_t pos = (uint32_t)tok_pos[t];
+    const uint32_t f = __umulhi(pos, cl.r_lo) + pos * cl.r_hi;
+    return (float)f * 2.3283064365386963e-10f;  // 2^-32
   }
   __device__ void operator()(int64_t row, int64_t, float x, float xp, const Col& cl) const {
     const int64_t t = tok_base + row;
@@ -102,9 +126,8 @@ struct QkvEpi {
     const int seg = cl.seg;
     const int64_t c = cl.c;
     float y = x;
-    if (cl.rev > 0.0) {
-      const double a = (double)tok_pos[t] * cl.rev;
-      const float r = (float)(a - floor(a));           // revolutions in [0, 1)
+    if (cl.rot) {
+      const float r = turn(t, cl);
       const float sn = __builtin_amdgcn_sinf(r), cs = __builtin_amdgcn_cosf(r);
       // (e, o) -> (e cos - o sin, e sin + o cos); the partner holds the other half
       y = cl.odd ? fmaf(xp, sn, x * cs) : fmaf(-xp, sn, x * cs);
@@ -121,6 +144,35 @@ struct QkvEpi {
       }
       __bf16* cdst = reinterpret_cast<__bf16*>(seg == 1 ? cache_k : cache_v);
       cdst[((int64_t)b * cache_cap + cr) * kc + c] = yb;
+      if (seg == 1 && c == 0 && cache_len) atomicMax(cache_len + b, cr + 1);
+    }
+  }
+  // columns c (even, described by cl) and c + 1 of a row: one rotation, and
+  // both values in one 4-byte store
+  __device__ void pair(int64_t row, int64_t, float x0, float x1, const Col& cl) const {
+    const int64_t t = tok_base + row;
+    const int64_t qc = (int64_t)H * D, kc = (int64_t)Hkv * D;
+    const int seg = cl.seg;
+    const int64_t c = cl.c;
+    float y0 = x0, y1 = x1;
+    if (cl.rot) {
+      const float r = turn(t, cl);
+      const float sn = __builtin_amdgcn_sinf(r), cs = __builtin_amdgcn_cosf(r);
+      y0 = fmaf(-x1, sn, x0 * cs);
+      y1 = fmaf(x0, sn, x1 * cs);
+    }
+    const uint32_t w = focus::pack_bf16x2(y0, y1);
+    uint32_t* dst = reinterpret_cast<uint32_t*>(seg == 0 ? q : seg == 1 ? k : v);
+    dst[(row * (seg == 0 ? qc : kc) + c) >> 1] = w;
+    if (seg > 0 && cache_k && tok_kind[t] == FOCUS_TOK_SUMMARY) {
+      const int32_t cr = tok_kmer[t];
+      const int32_t b = win_seq[tok_win[t]];
+      if (cr < 0 || cr >= cache_cap || b < 0 || b >= batch) {
+        focus::raise_err(err, FOCUS_ERR_CAPACITY);
+        return;
+      }
+      uint32_t* cdst = reinterpret_cast<uint32_t*>(seg == 1 ? cache_k : cache_v);
+      cdst[(((int64_t)b * cache_cap + cr) * kc + c) >> 1] = w;
       if (seg == 1 && c == 0 && cache_len) atomicMax(cache_len + b, cr + 1);
     }
   }
@@ -408,7 +460,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_wide(focus_gemm_desc d,
   //   acc[i][j][v] = C[m0 + wm + 32 i + 8 (v / 4) + 4 g + v % 4][n0 + wn + 32 j + l32]
   float* ct = reinterpret_cast<float*>(wave == 0 ? st0 : wave == 1 ? st1 : wave == 2 ? st2 : st3);
   const int64_t c0 = n0 + wn + 2 * lane;
-  const typename Epi::Col cl0 = epi.col(c0), cl1 = epi.col(c0 + 1);
+  const typename Epi::Col cl0 = epi.col(c0);
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
 #pragma unroll
@@ -422,8 +474,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_wide(focus_gemm_desc d,
     for (int r = 0; r < rows; ++r) {
       const float2 x = reinterpret_cast<const float2*>(ct)[r * 64 + lane];
       const int64_t row = m0 + wm + 64 * h + r;
-      epi(row, c0, x.x, x.y, cl0);
-      epi(row, c0 + 1, x.y, x.x, cl1);
+      epi.pair(row, c0, x.x, x.y, cl0);
     }
   }
 }
@@ -479,6 +530,10 @@ extern "C" focus_status focus_qkv_project(const focus_qkv_desc* q, focus_stream_
   if (q->cache_k && q->cache_cap < q->totals.max_cache_per_seq && q->tok_base == 0 && q->n_rows == q->totals.n_tokens)
     return FOCUS_E_CAPACITY;
   if (!focus::aligned16(q->hidden) || !focus::aligned16(q->w_qkv)) return FOCUS_E_ARG;
+  // pairs of bf16 columns are stored as one 4-byte word
+  if ((reinterpret_cast<uintptr_t>(q->q) | reinterpret_cast<uintptr_t>(q->k) | reinterpret_cast<uintptr_t>(q->v) |
+       reinterpret_cast<uintptr_t>(q->cache_k) | reinterpret_cast<uintptr_t>(q->cache_v)) & 3u)
+    return FOCUS_E_ARG;
   focus_gemm_desc g = {};
   g.m = q->n_rows;
   g.n = n;
