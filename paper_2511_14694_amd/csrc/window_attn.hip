@@ -491,6 +491,266 @@ __global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_d
   }
 }
 
+// --------------------------------------- bf16 MFMA, summary queries under C(t)
+
+// The adapter attention under C(t) with several windows per wave: G listed
+// windows in a row (list entries G gi .. G gi + G - 1) put their summaries in
+// the wave's 32 query slots (window k's B_k summaries at slots off_k ..
+// off_k + B_k - 1, off_k = B_0 + ... + B_{k-1}).  A pass covers a run of the
+// group's windows on one sequence: that sequence's cache rows [0, max C) once,
+// a row visible to a slot while it is below the slot's own window's C_w (the
+// caches of consecutive windows are prefixes of each other), then each
+// window's rows [0, its last summary's row], visible to that window's slots up
+// to the slot's own row.  So the cache prefix is streamed once for G windows,
+// and 32 slots hold G B_w queries instead of B_w.  Keys move in 32-row tiles
+// through two LDS stages (32 KB: five workgroups of one wave per CU).
+template <int D>
+__global__ __launch_bounds__(64) void attn_sq_group(focus_attn_desc d, float sc, int64_t n_pairs, int64_t nwl, int G,
+                                                    SumQ sq) {
+  constexpr int kBK = 32, kRB = D * 2, kTile = kBK * kRB, kCh16 = kRB / 16;
+  constexpr int kKsteps = D / 16, kDtiles = D / 32;
+  constexpr int kDma = kTile / 1024;  // wave copies per tile and tensor
+  constexpr int kRPK = 1024 / kRB;    // tile rows per wave copy
+  __shared__ __attribute__((aligned(1024))) char kbuf0[kTile], kbuf1[kTile];
+  __shared__ __attribute__((aligned(1024))) char vbuf0[kTile], vbuf1[kTile];
+  // per window of the group: window id, T, C_w, sequence, summaries, slot offset
+  __shared__ int64_t wg_win[32], wg_tok0[32], wg_s0[32];
+  __shared__ int wg_C[32], wg_b[32], wg_ns[32], wg_off[32], wg_nwk[32];
+
+  const int lane = threadIdx.x, l32 = lane & 31, g = lane >> 5;
+  const Item it = map_block(blockIdx.x, n_pairs, d.n_heads, 1);
+  if (!it.valid) return;
+  const int H = d.n_heads, Hkv = d.n_kv_heads, h = it.h;
+  const int hk = h / (H / Hkv);
+  const int64_t li0 = it.list_idx * G;
+  const int nk = (int)min((int64_t)G, nwl - li0);  // windows in this group
+  if (nk <= 0) return;
+
+  // lane k < nk reads window k's description; slot offsets by a prefix sum
+  bool bad = false;
+  if (lane < nk) {
+    const int64_t gw = listed_window(d, li0 + lane);
+    if (gw < 0 || gw >= d.totals.n_windows) {
+      bad = true;
+    } else {
+      const int T = d.win_ntok[gw], C = d.win_cache_off[gw], b = d.win_seq[gw], ns = sq.win_nsum[gw];
+      const int64_t tok0 = d.win_tok_off[gw] - d.qkv_tok_base, s0 = sq.win_sum_off[gw];
+      bad = b < 0 || b >= d.batch || C < 0 || C > d.cache_cap || tok0 < 0 || tok0 + T > d.qkv_rows || ns < 0 ||
+            ns > T || s0 < sq.base || s0 + ns > sq.base + sq.rows;
+      if (!bad) {
+        wg_win[lane] = gw;
+        wg_tok0[lane] = tok0;
+        wg_s0[lane] = s0;
+        wg_C[lane] = C;
+        wg_b[lane] = b;
+        wg_ns[lane] = ns;
+        // keys of the window phase: rows up to the last summary's
+        int nwk = 0;
+        if (ns > 0) {
+          const int64_t r = sq.sum_tok[s0 + ns - 1] - d.win_tok_off[gw];
+          nwk = (int)(r < 0 ? 0 : r >= T ? T - 1 : r) + 1;
+        }
+        wg_nwk[lane] = nwk;
+      }
+    }
+  }
+  if (__any(bad)) {
+    if (lane == 0) focus::raise_err(d.err, FOCUS_ERR_BOUNDS);
+    return;
+  }
+  if (lane == 0) {
+    int off = 0;
+    for (int k = 0; k < nk; ++k) {
+      wg_off[k] = off;
+      off += wg_ns[k];
+    }
+    if (off > 32) focus::raise_err(d.err, FOCUS_ERR_BOUNDS);  // more summaries than slots
+  }
+  __syncthreads();
+
+  // this lane's slot: window kl, its summary (global index s), window row pos
+  int kl = -1, pos = 0;
+  int64_t s = 0;
+  for (int k = 0; k < nk; ++k)
+    if (l32 >= wg_off[k] && l32 < wg_off[k] + wg_ns[k]) kl = k;
+  if (kl >= 0) {
+    s = wg_s0[kl] + (l32 - wg_off[kl]);
+    const int64_t r = sq.sum_tok[s] - d.win_tok_off[wg_win[kl]];
+    pos = (int)min(max(r, (int64_t)0), (int64_t)wg_nwk[kl] - 1);
+  }
+  const int Cl = kl >= 0 ? wg_C[kl] : 0;
+  // an unused slot (its result is dropped) sees every key of every phase, so
+  // it forces no masking
+  constexpr int kAll = 1 << 30;
+
+  // Q^T as the B operand: lane holds slot l32, head_dim [16 s + 8 g, +8)
+  bf16x8 qf[kKsteps];
+  {
+    const int64_t qrow = (kl >= 0 ? s : wg_s0[0]) - sq.base;
+    const bf16x8* qp =
+        reinterpret_cast<const bf16x8*>(reinterpret_cast<const __bf16*>(sq.q) + (qrow * H + h) * D);
+#pragma unroll
+    for (int k = 0; k < kKsteps; ++k) qf[k] = qp[2 * k + g];
+  }
+
+  const uint32_t row_bytes = (uint32_t)(Hkv * D * 2);
+  uint32_t rowb[kDma], kchunk[kDma], vchunk[kDma];
+#pragma unroll
+  for (int i = 0; i < kDma; ++i) {
+    const int r = i * kRPK + lane / kCh16;
+    const int p = lane % kCh16;
+    const int f = D == 128 ? (r & 3) : ((r >> 1) & 1);
+    rowb[i] = (uint32_t)r * row_bytes;
+    kchunk[i] = (uint32_t)((p ^ (r % kCh16)) * 16);
+    vchunk[i] = (uint32_t)((((p >> 2) ^ f) * 4 + (p & 3)) * 16);
+  }
+
+  f32x16 oacc[kDtiles];
+#pragma unroll
+  for (int dt = 0; dt < kDtiles; ++dt)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) oacc[dt][v] = 0.f;
+  float m_run = kMinit, l_run = 0.f;
+  const int grp = lane >> 4, ri = (lane >> 2) & 3, bq = lane & 3;
+
+  // rows [row0, row0 + 32) of the K/V rows at (kbase, vbase), nvalid of them
+  // real (the rest repeat the last one and are masked)
+  auto issue = [&](const char* kbase, const char* vbase, int row0, int nvalid, char* kt, char* vt) __attribute__((always_inline)) {
+    const uint32_t last = (uint32_t)(nvalid - 1 - row0) * row_bytes;
+    const char* kb = kbase + (int64_t)row0 * row_bytes;
+    const char* vb = vbase + (int64_t)row0 * row_bytes;
+#pragma unroll
+    for (int i = 0; i < kDma; ++i) {
+      const uint32_t rb = nvalid - row0 >= kBK ? rowb[i] : min(rowb[i], last);
+      const char* ks = kb + (rb + kchunk[i]);
+      const char* vs = vb + (rb + vchunk[i]);
+      __builtin_amdgcn_global_load_lds(ks, (lds_void*)(kt + i * 1024), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(vs, (lds_void*)(vt + i * 1024), 16, 0, 0);
+    }
+  };
+  // one 32-key tile: tile key kk is visible to this lane iff kk <= lim
+  auto compute = [&](const char* kt, const char* vt, int lim, bool need_mask) __attribute__((always_inline)) {
+    f32x16 sacc;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) sacc[v] = 0.f;
+#pragma unroll
+    for (int k = 0; k < kKsteps; ++k)
+      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(kt + k_off<D>(l32, 2 * k + g)),
+                                                     qf[k], sacc, 0, 0, 0);
+    // sacc[v] = score of slot l32 with tile key 8 (v/4) + 4 g + v%4
+    if (need_mask) {
+      const int lim_g = lim - 4 * g;
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+        if ((v >> 2) * 8 + (v & 3) > lim_g) sacc[v] = -INFINITY;
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[v]);
+    {
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+      mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));  // with lane ^ 32
+    }
+    const float m_new = fmaxf(m_run, mx * sc);
+    if (__any(m_new - m_run > kLazy)) {
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < kDtiles; ++dt)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) oacc[dt][v] *= alpha;
+      m_run = m_new;
+    }
+    float psum = 0.f;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const float p = __builtin_amdgcn_exp2f(fmaf(sacc[v], sc, -m_run));
+      sacc[v] = p;
+      psum += p;
+    }
+    l_run += psum;
+#pragma unroll
+    for (int m = 0; m < 2; ++m) {
+      bf16x8 pb;
+#pragma unroll
+      for (int v = 0; v < 8; ++v) pb[v] = (__bf16)sacc[8 * m + v];
+      // keys of B slot v: 16 m + 8 (v/4) + 4 g + v%4
+      const int kb = 16 * m + 4 * (grp >> 1) + ri;
+#pragma unroll
+      for (int dt = 0; dt < kDtiles; ++dt) {
+        const int col_byte = 2 * (32 * dt + 16 * (grp & 1) + 4 * bq);
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vt + v_off<D>(kb, col_byte)));
+        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vt + v_off<D>(kb + 8, col_byte)));
+        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7),
+                                                           pb, oacc[dt], 0, 0, 0);
+      }
+    }
+  };
+  // A phase: nrows rows at (kbase, vbase); this lane sees rows <= hi_l;
+  // tiles past every lane's hi are skipped.  Two stages, the barrier closing
+  // each step also waits for the next tile's copies.
+  auto phase = [&](const char* kbase, const char* vbase, int nrows, int hi_l) __attribute__((always_inline)) {
+    int hi_min = hi_l, hi_max = hi_l;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      hi_min = min(hi_min, __shfl_xor(hi_min, o));
+      hi_max = max(hi_max, __shfl_xor(hi_max, o));
+    }
+    const int ntl = (min(nrows, hi_max + 1) + kBK - 1) / kBK;
+    if (ntl <= 0) return;
+    issue(kbase, vbase, 0, nrows, kbuf0, vbuf0);
+    __syncthreads();
+    for (int t = 0; t < ntl; t += 2) {
+      if (t + 1 < ntl) issue(kbase, vbase, (t + 1) * kBK, nrows, kbuf1, vbuf1);
+      compute(kbuf0, vbuf0, hi_l - t * kBK, t * kBK + kBK - 1 > hi_min);
+      __syncthreads();
+      if (t + 1 >= ntl) break;
+      if (t + 2 < ntl) issue(kbase, vbase, (t + 2) * kBK, nrows, kbuf0, vbuf0);
+      compute(kbuf1, vbuf1, hi_l - (t + 1) * kBK, (t + 1) * kBK + kBK - 1 > hi_min);
+      __syncthreads();
+    }
+  };
+
+  const char* kwin_all = reinterpret_cast<const char*>(reinterpret_cast<const __bf16*>(d.k) + (int64_t)hk * D);
+  const char* vwin_all = reinterpret_cast<const char*>(reinterpret_cast<const __bf16*>(d.v) + (int64_t)hk * D);
+  for (int k0 = 0; k0 < nk;) {
+    // run [k0, k1) of windows on sequence b
+    const int b = wg_b[k0];
+    int k1 = k0 + 1, cmax = wg_C[k0];
+    while (k1 < nk && wg_b[k1] == b) cmax = max(cmax, wg_C[k1++]);
+    if (cmax > 0) {
+      const char* kc = reinterpret_cast<const char*>(reinterpret_cast<const __bf16*>(d.cache_k) +
+                                                     ((int64_t)b * d.cache_cap * Hkv + hk) * D);
+      const char* vc = reinterpret_cast<const char*>(reinterpret_cast<const __bf16*>(d.cache_v) +
+                                                     ((int64_t)b * d.cache_cap * Hkv + hk) * D);
+      phase(kc, vc, cmax, kl < 0 ? kAll : (kl >= k0 && kl < k1) ? Cl - 1 : -1);
+    }
+    for (int k = k0; k < k1; ++k) {
+      const int64_t tok0 = wg_tok0[k];
+      phase(kwin_all + tok0 * row_bytes, vwin_all + tok0 * row_bytes, wg_nwk[k], kl < 0 ? kAll : kl == k ? pos : -1);
+    }
+    k0 = k1;
+  }
+
+  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  if (kl >= 0) {
+    const float inv = 1.f / l_tot;
+    const int64_t orow = s - sq.base;
+    __bf16* op = reinterpret_cast<__bf16*>(sq.o) + (orow * H + h) * D;
+#pragma unroll
+    for (int dt = 0; dt < kDtiles; ++dt)
+#pragma unroll
+      for (int v4 = 0; v4 < 4; ++v4) {
+        // oacc[dt][4 v4 + e] = O[slot][32 dt + 8 v4 + 4 g + e]
+        uint2 w;
+        w.x = focus::pack_bf16x2(oacc[dt][4 * v4 + 0] * inv, oacc[dt][4 * v4 + 1] * inv);
+        w.y = focus::pack_bf16x2(oacc[dt][4 * v4 + 2] * inv, oacc[dt][4 * v4 + 3] * inv);
+        *reinterpret_cast<uint2*>(op + 32 * dt + 8 * v4 + 4 * g) = w;
+      }
+    if (g == 0 && sq.lse) sq.lse[orow * H + h] = (m_run + log2f(l_tot)) * kLn2;
+  }
+}
+
 // ----------------------------------------------------------------- f32 VALU
 
 template <int D, bool KL>
@@ -730,13 +990,26 @@ extern "C" focus_status focus_adapter_attn(const focus_adapter_desc* a, focus_st
 
   const float scale = a->softmax_scale > 0.f ? a->softmax_scale : 1.0f / sqrtf((float)a->head_dim);
   const float sc = scale * kLog2e;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const bool kl = a->mask == FOCUS_MASK_KMER_LOCAL;
+  if (!kl && t.max_window_summaries <= 32) {
+    // C(t): G windows per wave
+    const int G = (int)(32 / t.max_window_summaries);
+    const int64_t n_groups = focus::ceil_div(nwl, G);
+    const int64_t n_pairs_g = n_groups * a->n_heads;
+    const int64_t blocks_g = focus::ceil_div(n_pairs_g, focus::kXcds) * focus::kXcds;
+    if (blocks_g * 64 >= ((int64_t)1 << 32)) return FOCUS_E_SHAPE;
+    if (a->head_dim == 128)
+      hipLaunchKernelGGL((attn_sq_group<128>), dim3((uint32_t)blocks_g), dim3(64), 0, s, d, sc, n_pairs_g, nwl, G, sq);
+    else
+      hipLaunchKernelGGL((attn_sq_group<64>), dim3((uint32_t)blocks_g), dim3(64), 0, s, d, sc, n_pairs_g, nwl, G, sq);
+    return focus::launch_status();
+  }
   const int64_t n_pairs = nwl * a->n_heads;
   const int64_t qt = focus::ceil_div(t.max_window_summaries, 32);
   const int64_t blocks = focus::ceil_div(n_pairs, focus::kXcds) * focus::kXcds * qt;
   if (blocks * 64 >= ((int64_t)1 << 32) || qt > INT32_MAX) return FOCUS_E_SHAPE;
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const dim3 grid((uint32_t)blocks), block(64);
-  const bool kl = a->mask == FOCUS_MASK_KMER_LOCAL;
 #define FOCUS_SQ_LAUNCH(KERNEL) hipLaunchKernelGGL(KERNEL, grid, block, 0, s, d, sc, n_pairs, (int)qt, sq)
   if (a->head_dim == 128) {
     if (kl) FOCUS_SQ_LAUNCH((attn_bf16<128, 1, true, true>)); else FOCUS_SQ_LAUNCH((attn_bf16<128, 1, false, true>));
