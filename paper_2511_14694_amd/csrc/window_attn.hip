@@ -145,9 +145,13 @@ struct SumQ {
   int64_t base, rows;
 };
 
+// Under C(t) the workgroup has one more wave, which only copies tiles.
+template <bool KL, bool SQ>
+constexpr int producer_waves() { return (!KL && !SQ) ? 1 : 0; }
+
 template <int D, int W, bool KL, bool SQ>
-__global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_desc d, float sc, int64_t n_pairs, int QT,
-                                                       SumQ sq) {
+__global__ __launch_bounds__(64 * (W + producer_waves<KL, SQ>()), (W == 1 || producer_waves<KL, SQ>()) ? 1 : 2) void attn_bf16(
+    focus_attn_desc d, float sc, int64_t n_pairs, int QT, SumQ sq) {
   using C = Cfg<D, W>;
   // Two K and two V tile buffers as separate arrays, referenced statically by
   // a loop unrolled by two: the compiler can then tell a tile being read from
@@ -345,15 +349,25 @@ __global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_d
       for (int st = 0; st < 2; ++st)
 #pragma unroll
         for (int v = 0; v < 16; ++v) sacc[st][v] = 0.f;
+      // Per-lane LDS offsets are rebuilt each step behind an empty asm
+      // statement: not hoisted out of the loop once per buffer (registers),
+      // and one offset from the buffer, so the compiler still tells the
+      // buffers apart.  K row 32 st + l32, chunk 2 s + g sits at chunk
+      // (2 s + g) ^ (l32 mod kCh16) = 2 s ^ kx.
+      const int kx = g ^ (l32 & (C::kCh16 - 1));
+      auto kread = [&](int s, int st) {
+        int ko = l32 * C::kRB + (((2 * s) ^ kx) << 4);
+        asm volatile("" : "+v"(ko));
+        return *reinterpret_cast<const bf16x8*>(kl + (ko + st * 32 * C::kRB));
+      };
       bf16x8 ka[2], kn[2];
 #pragma unroll
-      for (int st = 0; st < 2; ++st) ka[st] = *reinterpret_cast<const bf16x8*>(kl + k_off<D>(st * 32 + l32, g));
+      for (int st = 0; st < 2; ++st) ka[st] = kread(0, st);
 #pragma unroll
       for (int s = 0; s < C::kKsteps; ++s) {
         if (s + 1 < C::kKsteps) {
 #pragma unroll
-          for (int st = 0; st < 2; ++st)
-            kn[st] = *reinterpret_cast<const bf16x8*>(kl + k_off<D>(st * 32 + l32, 2 * (s + 1) + g));
+          for (int st = 0; st < 2; ++st) kn[st] = kread(s + 1, st);
         }
 #pragma unroll
         for (int st = 0; st < 2; ++st) sacc[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[st], qf[s], sacc[st], 0, 0, 0);
@@ -408,14 +422,17 @@ __global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_d
 #pragma unroll
           for (int v = 0; v < 8; ++v) pb[v] = (__bf16)sacc[st][8 * m + v];
           // keys of B slot v: 32 st + 16 m + 8 (v/4) + 4 g + v%4
-          const int kb = st * 32 + 16 * m + 4 * (grp >> 1) + ri;
+          // V^T operand: row 32 st + 16 m + 4 (grp / 2) + ri (+ 8 for the
+          // upper half), byte 64 dt + 32 (grp & 1) + 8 bq of it, whose 64-byte
+          // granule sits at dt ^ f (f = ri, or ri / 2 for D = 64)
+          const int r0 = (st * 32 + 16 * m) * C::kRB;
 #pragma unroll
           for (int dt = 0; dt < C::kDtiles; ++dt) {
-            const int col_byte = 2 * (32 * dt + 16 * (grp & 1) + 4 * bq);
-            const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-                (lds_bf16x4*)(vl + v_off<D>(kb, col_byte)));
-            const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-                (lds_bf16x4*)(vl + v_off<D>(kb + 8, col_byte)));
+            int vo = (4 * (grp >> 1) + ri) * C::kRB + 32 * (grp & 1) + 8 * bq +
+                     ((dt ^ (D == 128 ? ri : (ri >> 1) & 1)) << 6);
+            asm volatile("" : "+v"(vo));
+            const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vl + (vo + r0)));
+            const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vl + (vo + r0 + 8 * C::kRB)));
             const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
             oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, oacc[dt], 0, 0, 0);
           }
@@ -438,37 +455,71 @@ __global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_d
       __syncthreads();
     }
   } else {
-    // Tile t lives in buffers t % 3.  Step t first starts the copies of tile
-    // t + 2 (into the buffers tile t - 1 left; past the last tile it copies
-    // the last tile again, into a buffer no later step reads), and ends by
-    // waiting until only those copies are in flight (tile t + 1 has landed),
-    // then a barrier: a copy has two steps to land.  The signal fences keep
-    // the compiler from moving memory accesses across the wait and barrier.
-    auto end_step = [&]() {
-      constexpr int kVm = 2 * kDma;  // s_waitcnt vmcnt(kVm) expcnt(7) lgkmcnt(0)
+    // Tile t lives in buffers t % 3.  The extra wave (wave W) does all the
+    // copying: step t starts the copies of tile t + 2 (into the buffers tile
+    // t - 1 left; past the last tile it copies the last tile again, into a
+    // buffer no later step reads) and ends by waiting until only those are in
+    // flight (tile t + 1 has landed); the W computing waves never wait on a
+    // copy, and a barrier closes every step for all W + 1.  (A wave stalls
+    // while the address unit takes its copies, one 1 KB wave copy at a time:
+    // here that is the copying wave alone.)  The signal fences keep the
+    // compiler from moving memory accesses across the wait and barrier.
+    constexpr int kAll = kDma * W;  // wave copies per tile and tensor
+    auto end_step = [&](bool copying) {
+      constexpr int kVm = 2 * kAll;  // s_waitcnt vmcnt(kVm) expcnt(7) lgkmcnt(0)
       __atomic_signal_fence(__ATOMIC_SEQ_CST);
-      __builtin_amdgcn_s_waitcnt((kVm & 15) | ((kVm >> 4) << 14) | (7 << 4) | (0 << 8));
+      if (copying)
+        __builtin_amdgcn_s_waitcnt((kVm & 15) | ((kVm >> 4) << 14) | (7 << 4) | (0 << 8));
+      else
+        __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4) | (0 << 8));  // lgkmcnt(0)
       __builtin_amdgcn_s_barrier();
       __atomic_signal_fence(__ATOMIC_SEQ_CST);
     };
-    issue_tile(0, kbuf0, vbuf0);
-    issue_tile(min(1, ntiles - 1), kbuf1, vbuf1);
-    __syncthreads();  // tiles 0 and 1 have landed (a full wait: the compiler
-                      // then knows no copy is pending when the loop starts)
-    for (int t = 0; t < ntiles; t += 3) {
-      issue_tile(min(t + 2, ntiles - 1), kbuf2, vbuf2);
-      compute_tile(t, kbuf0, vbuf0);
-      end_step();
-      if (t + 1 >= ntiles) break;
-      issue_tile(min(t + 3, ntiles - 1), kbuf0, vbuf0);
-      compute_tile(t + 1, kbuf1, vbuf1);
-      end_step();
-      if (t + 2 >= ntiles) break;
-      issue_tile(min(t + 4, ntiles - 1), kbuf1, vbuf1);
-      compute_tile(t + 2, kbuf2, vbuf2);
-      end_step();
+    if (wave == W) {
+      // all kAll wave copies of a tensor: rows i kRPK + lane / kCh16.  (This
+      // wave reads no LDS, so its buffers may be chosen at run time.)
+      auto copy_tile = [&](int t, char* kbuf, char* vbuf) {
+        const bool in_cache = t < nct;
+        const int row0 = in_cache ? t * C::kBK : (t - nct) * C::kBK;
+        const int nvalid = (in_cache ? Cw : nwk) - row0;
+        const char* kb = (in_cache ? kcache : kwin) + (int64_t)row0 * row_bytes;
+        const char* vb = (in_cache ? vcache : vwin) + (int64_t)row0 * row_bytes;
+        const uint32_t last = (uint32_t)(nvalid - 1) * row_bytes;
+        const int lr = lane / C::kCh16, p = lane % C::kCh16;
+#pragma unroll
+        for (int i = 0; i < kAll; ++i) {
+          const int r = i * kRPK + lr;
+          const int f = D == 128 ? (r & 3) : ((r >> 1) & 1);
+          const uint32_t rb = min((uint32_t)r * row_bytes, last);
+          const char* ks = kb + (rb + (uint32_t)((p ^ (r % C::kCh16)) * 16));
+          const char* vs = vb + (rb + (uint32_t)((((p >> 2) ^ f) * 4 + (p & 3)) * 16));
+          __builtin_amdgcn_global_load_lds(ks, (lds_void*)(kbuf + i * 1024), 16, 0, 0);
+          __builtin_amdgcn_global_load_lds(vs, (lds_void*)(vbuf + i * 1024), 16, 0, 0);
+        }
+      };
+      copy_tile(0, kbuf0, vbuf0);
+      copy_tile(min(1, ntiles - 1), kbuf1, vbuf1);
+      __syncthreads();  // tiles 0 and 1 have landed
+      for (int t = 0; t < ntiles; ++t) {
+        const int nb = (t + 2) % 3;
+        copy_tile(min(t + 2, ntiles - 1), nb == 0 ? kbuf0 : nb == 1 ? kbuf1 : kbuf2,
+                  nb == 0 ? vbuf0 : nb == 1 ? vbuf1 : vbuf2);
+        end_step(true);
+      }
+      __builtin_amdgcn_s_waitcnt(0);  // no copy into LDS outlives the block
+      return;
     }
-    __builtin_amdgcn_s_waitcnt(0);  // no copy into LDS outlives the block
+    __syncthreads();
+    for (int t = 0; t < ntiles; t += 3) {
+      compute_tile(t, kbuf0, vbuf0);
+      end_step(false);
+      if (t + 1 >= ntiles) break;
+      compute_tile(t + 1, kbuf1, vbuf1);
+      end_step(false);
+      if (t + 2 >= ntiles) break;
+      compute_tile(t + 2, kbuf2, vbuf2);
+      end_step(false);
+    }
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
@@ -910,7 +961,8 @@ extern "C" focus_status focus_window_attn(const focus_attn_desc* d, focus_stream
   const bool kl = d->mask == FOCUS_MASK_KMER_LOCAL;
   const int waves = kl ? kBf16WavesKL : kBf16Waves;
   const int bq = d->dtype == FOCUS_BF16 ? 32 * waves : 64;
-  const int threads = d->dtype == FOCUS_BF16 ? 64 * waves : 256;
+  // (C(t): one more wave, which copies the tiles)
+  const int threads = d->dtype == FOCUS_BF16 ? 64 * (waves + (kl ? 0 : 1)) : 256;
   const int64_t qt = focus::ceil_div(t.max_window_tokens, bq);
   const int64_t blocks = focus::ceil_div(n_pairs, focus::kXcds) * focus::kXcds * qt;
   if (blocks * threads >= ((int64_t)1 << 32) || qt > INT32_MAX) return FOCUS_E_SHAPE;
