@@ -309,7 +309,9 @@ typedef struct {
   int32_t n_kv_heads;
   int32_t head_dim;             /* 64 or 128                                 */
   float softmax_scale;          /* <= 0: 1/sqrt(head_dim)                    */
-  int32_t split_keys;           /* keys per split, multiple of 16; 0 = auto  */
+  int32_t split_keys;           /* keys per split, multiple of 16; 0 = auto:
+                                   batch x capacity spread over about 7/8 of
+                                   the current device's compute units        */
   int32_t reserved;
   const void* q;                /* [batch, n_heads, head_dim]                */
   const void* k_new;            /* [batch, n_kv_heads, head_dim]             */
