@@ -5,13 +5,15 @@
 // Q/K/V projection).  a_rows gathers A's rows, so the summary tokens' queries
 // are projected without first copying their hidden states.
 //
-// One workgroup = 4 waves = a 128 x 128 tile of C; each wave owns 64 x 64 as
-// 2 x 2 blocks of v_mfma_f32_32x32x16_bf16.  K advances 64 at a time through
-// LDS, double-buffered, copied global -> LDS directly (global_load_lds, 16 B
-// per lane; the A copy gathers rows per lane).  A is read with ds_read_b128
-// from 128-byte rows whose 16-byte chunks are XOR-swizzled by row; B (row-
-// major [K, N]) is read k-major with the transposing ds_read_b64_tr_b16 from
-// 256-byte rows whose 64-byte granules are XOR-swizzled, as the attention's V.
+// Two tile shapes (the large one is described at gemm_bf16_wide).  The
+// general one: one workgroup = 4 waves = a 128 x 128 tile of C; each wave owns
+// 64 x 64 as 2 x 2 blocks of v_mfma_f32_32x32x16_bf16.  K advances 64 at a
+// time through LDS, double-buffered, copied global -> LDS directly
+// (global_load_lds, 16 B per lane; the A copy gathers rows per lane).  A is
+// read with ds_read_b128 from 128-byte rows whose 16-byte chunks are
+// XOR-swizzled by row; B (row-major [K, N]) is read k-major with the
+// transposing ds_read_b64_tr_b16 from 256-byte rows whose 64-byte granules are
+// XOR-swizzled, as the attention's V.
 #include "common.h"
 
 namespace {
@@ -295,11 +297,12 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16(focus_gemm_desc d, int6
 
 
 // Large products (N a multiple of 256, M >= 256, K a multiple of 128): one
-// workgroup = 4 waves = a 256 x 256 tile of C, each wave 128 x 128 as 4 x 4
+// workgroup = 8 waves = a 256 x 256 tile of C, each wave 128 x 64 as 4 x 2
 // blocks of v_mfma_f32_32x32x16_bf16.  Per 16-deep k-step a wave reads 4 A and
-// 4 B operands from LDS for 16 MFMAs, half the LDS traffic per MFMA of the
-// 128 x 128 tile (whose 64 x 64 waves read 2 + 2 for 4); one wave per SIMD
-// (the 256 accumulators fill the AGPRs).  K advances 32 at a time through four
+// 2 B operands from LDS for 8 MFMAs (the 128 x 128 tile's 64 x 64 waves read
+// 2 + 2 for 4); two waves per SIMD, so one's LDS reads and barrier waits
+// overlap the other's MFMAs (four waves of 128 x 128, one per SIMD, ran 7 %
+// slower).  K advances 32 at a time through four
 // LDS stages (A 256 x 64 B + B 32 x 512 B = 32 KB each): the copies of step
 // t + 3 start in step t, so a copy has three steps to land, and a step ends on
 // a partial wait (only the two younger steps' copies in flight) plus a barrier.
@@ -312,9 +315,10 @@ constexpr int kBRow2 = kBN2 * 2;                 // bytes per B tile row (512)
 constexpr int kATile2 = kBM2 * kARow2;           // 16 KB
 constexpr int kBTile2 = kBK2 * kBRow2;           // 16 KB
 constexpr int kStage2 = kATile2 + kBTile2;       // A then B
+constexpr int kThreadsWide = 512;
 
 template <class Epi>
-__global__ __launch_bounds__(kThreads, 1) void gemm_bf16_wide(focus_gemm_desc d, int64_t m_tiles, Epi epi) {
+__global__ __launch_bounds__(kThreadsWide, 1) void gemm_bf16_wide(focus_gemm_desc d, int64_t m_tiles, Epi epi) {
   // One array per stage: the compiler tracks the copies in flight per array.
   __shared__ __attribute__((aligned(1024))) char st0[kStage2], st1[kStage2], st2[kStage2], st3[kStage2];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, l32 = lane & 31, g = lane >> 5;
@@ -323,18 +327,18 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_wide(focus_gemm_desc d,
   const int64_t gm_rows = min((int64_t)kGroupM, m_tiles - grp0 * kGroupM);
   const int64_t mt = grp0 * kGroupM + in_grp % gm_rows, nt = in_grp / gm_rows;
   const int64_t m0 = mt * kBM2, n0 = nt * kBN2;
-  const int wm = (wave & 1) * 128, wn = (wave >> 1) * 128;  // this wave's 128 x 128 in the tile
+  const int wm = (wave & 1) * 128, wn = (wave >> 1) * 64;  // this wave's 128 x 64 in the tile
 
-  // Copy plan: A tile = 16 wave-loads of 1 KB (16 rows x 64 B), 4 per wave;
-  // B tile = 16 wave-loads (2 rows x 512 B), 4 per wave.  Lane p of a row
+  // Copy plan: A tile = 16 wave-loads of 1 KB (16 rows x 64 B), 2 per wave;
+  // B tile = 16 wave-loads (2 rows x 512 B), 2 per wave.  Lane p of a row
   // fetches the global chunk the swizzled layout keeps at its slot.
   const char* A = reinterpret_cast<const char*>(d.a);
   const char* B = reinterpret_cast<const char*>(d.b);
   const int64_t a_ld = d.lda * 2, b_ld = d.ldb * 2;
-  const char* a_src[4];
+  const char* a_src[2];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int r = (wave * 4 + i) * 16 + (lane >> 2), p = lane & 3;  // A tile row, 16-B slot
+  for (int i = 0; i < 2; ++i) {
+    const int r = (wave * 2 + i) * 16 + (lane >> 2), p = lane & 3;  // A tile row, 16-B slot
     const int64_t gm = min(m0 + r, d.m - 1);                         // ragged M: repeat the last row
     int64_t ar = d.a_rows ? d.a_rows[gm] : gm;
     if (ar < 0 || ar >= d.a_nrows) {
@@ -343,36 +347,36 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_wide(focus_gemm_desc d,
     }
     a_src[i] = A + ar * a_ld + ((p ^ ((r >> 2) & 3)) << 4);
   }
-  // B tile row of wave-load i: (wave * 4 + i) * 2 + lane / 32 (row mod 4
+  // B tile row of wave-load i: (wave * 2 + i) * 2 + lane / 32 (row mod 4
   // alternates with i); slot lane % 32
   const int pb = lane & 31;
-  const int brow0 = wave * 8 + (lane >> 5);
+  const int brow0 = wave * 4 + (lane >> 5);
   const uint32_t b_col0 = (uint32_t)((((pb >> 2) ^ (brow0 & 3)) * 4 + (pb & 3)) * 16);
   const uint32_t b_col1 = (uint32_t)((((pb >> 2) ^ ((brow0 + 2) & 3)) * 4 + (pb & 3)) * 16);
   const char* b_src = B + (int64_t)brow0 * b_ld + n0 * 2;
 
   // wave copy pair i (A rows and B rows) of the step at k0 into a stage
   auto issue_pair = [&](int64_t k0, char* stage, int i) {
-    __builtin_amdgcn_global_load_lds(a_src[i] + k0 * 2, (lds_void*)(stage + (wave * 4 + i) * 1024), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(a_src[i] + k0 * 2, (lds_void*)(stage + (wave * 2 + i) * 1024), 16, 0, 0);
     const char* gb = b_src + (k0 + 2 * i) * b_ld + ((i & 1) ? b_col1 : b_col0);
-    __builtin_amdgcn_global_load_lds(gb, (lds_void*)(stage + kATile2 + (wave * 4 + i) * 1024), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(gb, (lds_void*)(stage + kATile2 + (wave * 2 + i) * 1024), 16, 0, 0);
   };
   auto issue = [&](int64_t k0, char* stage) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) issue_pair(k0, stage, i);
+    for (int i = 0; i < 2; ++i) issue_pair(k0, stage, i);
   };
 
-  f32x16 acc[4][4];
+  f32x16 acc[4][2];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
   // Computes the step in `stage` and starts the copies of the step at k_nxt
-  // into `nxt`, one pair after every 8 MFMAs: a wave that sends all its
-  // copies at once stalls until the address unit has taken them.
+  // into `nxt`, one pair after every 4 MFMAs of the first k-step: a wave that
+  // sends all its copies at once stalls until the address unit has taken them.
   auto compute = [&](const char* stage, int64_t k_nxt, char* nxt) {
     // Per-lane LDS offsets, rebuilt each step behind an empty asm statement
     // (not hoisted per stage; one offset from each stage, so the compiler can
@@ -381,24 +385,24 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_wide(focus_gemm_desc d,
     //   B: transposing read of rows 16 s + 8 (grp / 2) + ri (+ 4), byte
     //      2 (wn + 32 j + 16 (grp & 1) + 4 bq), granule ((wn / 32 + j) ^ ri)
     const int grp = lane >> 4, ri = (lane >> 2) & 3, bq = lane & 3;
-    int ao[2], bo[4];
+    int ao[2], bo[2];
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
       ao[s] = (wm + l32) * kARow2 + (((2 * s + g) ^ ((l32 >> 2) & 3)) << 4);
       asm volatile("" : "+v"(ao[s]));
     }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < 2; ++j) {
       bo[j] = kATile2 + (8 * (grp >> 1) + ri) * kBRow2 + ((((wn >> 5) + j) ^ ri) << 6) + 32 * (grp & 1) + 8 * bq;
       asm volatile("" : "+v"(bo[j]));
     }
-    // Operands of k-step s + 1 are read while the 16 MFMAs of k-step s run.
-    bf16x8 af[2][4], bf[2][4];
+    // Operands of k-step s + 1 are read while the 8 MFMAs of k-step s run.
+    bf16x8 af[2][4], bf[2][2];
     auto load = [&](int s, int buf) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) af[buf][i] = *reinterpret_cast<const bf16x8*>(stage + (ao[s] + 32 * i * kARow2));
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < 2; ++j) {
         const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(stage + (bo[j] + 16 * s * kBRow2)));
         const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(stage + (bo[j] + (16 * s + 4) * kBRow2)));
         bf[buf][j] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
@@ -411,11 +415,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_wide(focus_gemm_desc d,
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < 2; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s][i], bf[s][j], acc[i][j], 0, 0, 0);
-        if (i & 1) {
+        if (s == 0 && (i & 1)) {
           __builtin_amdgcn_sched_barrier(0);
-          issue_pair(k_nxt, nxt, 2 * s + (i >> 1));
+          issue_pair(k_nxt, nxt, i >> 1);
           __builtin_amdgcn_sched_barrier(0);
         }
       }
@@ -427,7 +431,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_wide(focus_gemm_desc d,
   // again), compute step t, wait until step t + 1 has landed, barrier.
   const int64_t nk = d.k / kBK2;
   auto end_step = [&]() {
-    constexpr int kVm = 2 * 8;  // two younger steps of 8 wave copies: vmcnt(16) expcnt(7) lgkmcnt(0)
+    constexpr int kVm = 2 * 4;  // two younger steps of 4 wave copies: vmcnt(8) expcnt(7) lgkmcnt(0)
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
     __builtin_amdgcn_s_waitcnt((kVm & 15) | ((kVm >> 4) << 14) | (7 << 4) | (0 << 8));
     __builtin_amdgcn_s_barrier();
@@ -452,27 +456,30 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_wide(focus_gemm_desc d,
   __builtin_amdgcn_s_waitcnt(0);  // no copy into LDS outlives the block
   __syncthreads();                // and no wave still reads a stage
 
-  // Epilogue through LDS: each wave parks 64 x 128 of its float32 results
-  // (half its tile) in one stage, then walks them a row at a time, a lane
-  // taking two adjacent columns (a RoPE pair): the epilogue code appears once
-  // and every store of a row is contiguous.  Same-wave LDS accesses complete
-  // in order, so no barrier is needed between the writes and the reads.
+  // Epilogue through LDS: each wave parks 64 x 64 of its float32 results
+  // (half its tile) in half a stage, then walks them two rows at a time (one
+  // per half-wave), a lane taking two adjacent columns (a RoPE pair): the
+  // epilogue code appears once and every store of a row is contiguous.
+  // Same-wave LDS accesses complete in order, so no barrier is needed between
+  // the writes and the reads.
   //   acc[i][j][v] = C[m0 + wm + 32 i + 8 (v / 4) + 4 g + v % 4][n0 + wn + 32 j + l32]
-  float* ct = reinterpret_cast<float*>(wave == 0 ? st0 : wave == 1 ? st1 : wave == 2 ? st2 : st3);
-  const int64_t c0 = n0 + wn + 2 * lane;
+  float* ct = reinterpret_cast<float*>((wave >> 1) == 0 ? st0 : (wave >> 1) == 1 ? st1 : (wave >> 1) == 2 ? st2 : st3) +
+              (wave & 1) * 64 * 64;
+  const int half = lane >> 5, cl32 = lane & 31;
+  const int64_t c0 = n0 + wn + 2 * cl32;
   const typename Epi::Col cl0 = epi.col(c0);
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
 #pragma unroll
     for (int i2 = 0; i2 < 2; ++i2)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int v = 0; v < 16; ++v)
-          ct[(32 * i2 + 8 * (v >> 2) + 4 * g + (v & 3)) * 128 + 32 * j + l32] = acc[2 * h + i2][j][v];
+          ct[(32 * i2 + 8 * (v >> 2) + 4 * g + (v & 3)) * 64 + 32 * j + l32] = acc[2 * h + i2][j][v];
     const int64_t rows = min((int64_t)64, d.m - (m0 + wm + 64 * h));
-    for (int r = 0; r < rows; ++r) {
-      const float2 x = reinterpret_cast<const float2*>(ct)[r * 64 + lane];
+    for (int r = half; r < rows; r += 2) {
+      const float2 x = reinterpret_cast<const float2*>(ct)[r * 32 + cl32];
       const int64_t row = m0 + wm + 64 * h + r;
       epi.pair(row, c0, x.x, x.y, cl0);
     }
@@ -486,7 +493,7 @@ focus_status launch_gemm(const focus_gemm_desc& d, const Epi& epi, focus_stream_
   if (d.n % kBN2 == 0 && d.m >= kBM2 && d.k % (4 * kBK2) == 0) {
     const int64_t m_tiles = focus::ceil_div(d.m, kBM2), n_tiles = d.n / kBN2;
     if (m_tiles * n_tiles > INT32_MAX) return FOCUS_E_SHAPE;
-    hipLaunchKernelGGL(gemm_bf16_wide<Epi>, dim3((uint32_t)(m_tiles * n_tiles)), dim3(kThreads), 0, s, d, m_tiles, epi);
+    hipLaunchKernelGGL(gemm_bf16_wide<Epi>, dim3((uint32_t)(m_tiles * n_tiles)), dim3(kThreadsWide), 0, s, d, m_tiles, epi);
   } else {
     const int64_t m_tiles = focus::ceil_div(d.m, kBM), n_tiles = d.n / kBN;
     if (m_tiles * n_tiles > INT32_MAX) return FOCUS_E_SHAPE;
