@@ -75,11 +75,14 @@ struct Item {
 // run together on an XCD then stream the same cache rows of one head at about
 // the same time, so each row is fetched into its L2 once for all of them.
 // Otherwise pair p = list_idx * H + h goes to XCD p % 8, in increasing p.
+// A pair's query tiles go last-first: under the causal window mask the last
+// tile sees the most keys, and starting the longest workgroups first shortens
+// the tail of a launch (a 32 000-token dense window: 8.6 -> 7.7 ms).
 __device__ inline Item map_block(int64_t bid, int64_t n_pairs, int H, int QT) {
   const int x = (int)(bid % focus::kXcds);
   const int64_t s = bid / focus::kXcds;
   Item it;
-  it.qt = (int)(s % QT);
+  it.qt = QT - 1 - (int)(s % QT);
   const int64_t j = s / QT;  // this XCD's j-th pair
   if (H % focus::kXcds == 0) {
     const int64_t nwl = n_pairs / H;  // listed windows
