@@ -5,7 +5,8 @@ the float64 oracle that stores bf16 as the device does.
 Every row of small layouts (ragged k, k = 0 windows, GQA, head_dim 64 / 128);
 sampled rows of the 1 Mb layout with an Evo-2-scale projection (d_model 4096,
 32 + 2 x 32 heads of 128), including positions near 1 M where the rotation
-angle must be reduced in double precision.  The fused cache write is checked
+angle (in revolutions) must keep its fraction to ~2^-32.  Outputs that are not
+4-byte aligned are refused.  The fused cache write is checked
 bit for bit against focus_compact_kv applied to the projected K / V, and
 cache_len against the summary counts.  Window-by-window calls reproduce the
 whole-layout call bit for bit.  Tolerance: the bf16 bar (max-abs 2e-2, rel-L2
@@ -114,3 +115,19 @@ def test_evo2_scale_projection_1mb_sampled():
     assert_parity(to64(v[idx]), rv, "bf16", "v 1 Mb")
     del q, k, v, hid
     torch.cuda.empty_cache()
+
+
+def test_projection_rejects_misaligned_outputs():
+    """Pairs of bf16 columns are stored as 4-byte words: q, k, v and the
+    caches must be 4-byte aligned."""
+    announce("projection misaligned q")
+    seq, W, kmer, H, Hkv, D, d = [1000], 500, 100, 2, 2, 64, 128
+    km, tot, lay, hid, w = _setup(seq, W, kmer, H, Hkv, D, d, 11)
+    rows = tot.n_tokens
+    buf = torch.empty(rows * H * D + 1, dtype=torch.bfloat16, device=DEV)
+    q_bad = buf[1:].view(rows, H, D)                # 2-byte offset
+    with pytest.raises(F.FocusError):
+        F.focus_qkv_project(lay, hid, w, H, Hkv, q=q_bad)
+    q_ok, _, _ = F.focus_qkv_project(lay, hid, w, H, Hkv)
+    torch.cuda.synchronize()
+    assert torch.isfinite(q_ok.float()).all()
