@@ -57,7 +57,7 @@ struct Sums {
     const float d = p - q;
     l1 += fabsf(d);
     l2 = fmaf(d, d, l2);
-    const float s = sqrtf(p) - sqrtf(q);
+    const float s = __builtin_amdgcn_sqrtf(p) - __builtin_amdgcn_sqrtf(q);  // p, q clipped: no denormals
     h = fmaf(s, s, h);
     const float lp = __builtin_amdgcn_logf(p), lq = __builtin_amdgcn_logf(q);
     const float lm = __builtin_amdgcn_logf(0.5f * (p + q));
@@ -232,7 +232,9 @@ __global__ __launch_bounds__(kThreads) void fid_rows_wave(focus_fidelity_desc d)
     const float dd = pn - qn;
     l1 += fabsf(dd);
     l2 = fmaf(dd, dd, l2);
-    const float sd = sqrtf(pn) - sqrtf(qn);
+    // pn, qn >= 1e-12 / 1.x after the clip: no denormals, so the bare
+    // v_sqrt_f32 (no denormal scaling around it) is exact to its ulp
+    const float sd = __builtin_amdgcn_sqrtf(pn) - __builtin_amdgcn_sqrtf(qn);
     h = fmaf(sd, sd, h);
     // log2 m from lp and lq (exactly lp when lp == lq, so identical inputs
     // give an exact zero): m = 2^max * (1 + 2^-|lp - lq|) / 2
