@@ -16,7 +16,9 @@
 //
 // bf16 path (the hot one): one workgroup = 8 waves (4 under the k-mer-local
 // mask) = 32 query rows per wave of one (window, head); keys stream in tiles
-// of 64 through LDS, double-buffered, copied global -> LDS directly:
+// of 64 through LDS, copied global -> LDS directly (under C(t) three buffers
+// and a ninth wave that does all the copying; otherwise two buffers, each wave
+// copying its share):
 //   S^T = K Q^T   v_mfma_f32_32x32x16_bf16: each lane ends up holding one
 //                 query's scores for 16 keys of a 32-key block, so the row
 //                 max / row sum are lane-local plus one exchange with lane^32;
@@ -31,6 +33,10 @@
 // (window, head) land on the same XCD (sharing K/V through its L2) and the
 // listed windows are started in list order (last window = largest cache first
 // by default).
+//
+// Summary queries (the FOCUS adapter's attention): under C(t) several windows'
+// summaries share one wave (attn_sq_group); otherwise the bf16 kernel above
+// runs with one wave of 32 summary slots per (window, head).
 //
 // f32 path: a plain VALU kernel (4 lanes per query row, exact online softmax),
 // used for the float32 checks; it is not tuned.
