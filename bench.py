@@ -449,15 +449,28 @@ def secondary_streaming(torch, F, s, n_windows=200):
     lay = s["lay"]
     nw = lay.totals.n_windows
     ids = [torch.tensor([w_], dtype=torch.int32, device="cuda:0") for w_ in range(nw - n_windows, nw)]
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for i in ids:
-        F.focus_window_attn(lay, s["q"], s["k"], s["v"], s["ck"], s["cv"], o=s["o"], lse=s["lse"], win_ids=i)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1)
-    return {"windows": n_windows, "ms_per_window": ms / n_windows,
-            "note": "one launch per window (the last windows, largest caches)"}
+    # key-split scratch (the same size for every single-window launch), allocated once
+    n_ws = F.focus_window_attn_workspace(lay, s["q"], s["k"], s["v"], s["ck"], s["cv"], ids[-1])
+    split_ws = torch.empty(max(n_ws, 16), dtype=torch.uint8, device="cuda:0")
+    no_split = torch.empty(0, dtype=torch.uint8, device="cuda:0")
+
+    def run(ws):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in ids:
+            F.focus_window_attn(lay, s["q"], s["k"], s["v"], s["ck"], s["cv"], o=s["o"], lse=s["lse"],
+                                win_ids=i, workspace=ws)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n_windows
+
+    run(split_ws)
+    ms = run(split_ws)
+    ms_unsplit = run(no_split)
+    return {"windows": n_windows, "ms_per_window": ms, "ms_per_window_unsplit": ms_unsplit,
+            "workspace_bytes": n_ws,
+            "note": "one launch per window (the last windows, largest caches); keys split over the "
+                    "compute units the 128 (head, query tile) items leave idle"}
 
 
 def main():

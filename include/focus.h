@@ -271,16 +271,25 @@ typedef struct {
   int64_t cache_cap;
   void* o;                      /* [qkv_rows, n_heads, head_dim], dtype      */
   float* lse;                   /* [qkv_rows, n_heads] float32, or NULL      */
-  void* workspace;              /* may be NULL if the size query returns 0   */
+  void* workspace;              /* optional key-split scratch (see below)    */
   size_t workspace_bytes;
   int32_t* err;
 } focus_attn_desc;
 
-/* Workspace bytes focus_window_attn needs for this descriptor (0 today). */
+/* Workspace bytes that let focus_window_attn split keys for this descriptor
+ * on the current device (0 when it would not split).  A bf16 C(t) launch whose
+ * (window, head, query tile) items are too few to occupy every compute unit
+ * (one window per call) splits each item's key tiles over n workgroups, which
+ * write unnormalised float32 partials to the workspace, merged by a second
+ * kernel through their log-sum-exp (results differ from the unsplit ones by
+ * float32 rounding only).  The workspace is optional: with d->workspace NULL,
+ * not 16-byte aligned or smaller than this, the launch runs unsplit.  It is
+ * scratch for the duration of the call; calls that share one on overlapping
+ * streams race. */
 size_t focus_window_attn_workspace(const focus_attn_desc* d);
-/* Errors: E_NULL, E_ARG, E_DTYPE, E_SHAPE, E_UNSUPPORTED, E_WORKSPACE,
- * E_CAPACITY (plan's max_window_cache > cache_cap), E_HIP.  A window whose rows
- * fall outside the buffers is skipped with FOCUS_ERR_BOUNDS. */
+/* Errors: E_NULL, E_ARG, E_DTYPE, E_SHAPE, E_UNSUPPORTED, E_CAPACITY (plan's
+ * max_window_cache > cache_cap), E_HIP.  A window whose rows fall outside the
+ * buffers is skipped with FOCUS_ERR_BOUNDS. */
 focus_status focus_window_attn(const focus_attn_desc* d, focus_stream_t stream);
 
 /* ------------------------------------------------------------------------ */

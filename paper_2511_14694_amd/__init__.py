@@ -216,13 +216,19 @@ def focus_window_attn(lay: Layout, q, k, v, cache_k=None, cache_v=None, o=None, 
                       mask: int = FOCUS_MASK_CT, workspace=None, want_lse: bool = True,
                       err=None, stream=None):
     """Window attention over [cache ; window] for the listed windows (all if
-    win_ids is None).  q [rows, H, D], k/v [rows, H_kv, D]; returns (o, lse)."""
+    win_ids is None).  q [rows, H, D], k/v [rows, H_kv, D]; returns (o, lse).
+    workspace None allocates what focus_window_attn_workspace asks for; an
+    empty tensor runs without the key split."""
     if o is None:
         o = torch.empty_like(q)
     if lse is None and want_lse:
         lse = torch.empty(q.shape[0], q.shape[1], dtype=torch.float32, device=q.device)
     if o.shape != q.shape or o.dtype != q.dtype or (lse is not None and tuple(lse.shape) != tuple(q.shape[:2])):
         raise ValueError("o must match q; lse must be [rows, heads]")
+    if workspace is None:
+        # key-split scratch for launches that would leave compute units idle
+        n = focus_window_attn_workspace(lay, q, k, v, cache_k, cache_v, win_ids)
+        workspace = torch.empty(n, dtype=torch.uint8, device=q.device) if n > 0 else None
     d = _attn_desc(lay, q, k, v, cache_k, cache_v, o, lse, win_ids, qkv_tok_base, softmax_scale,
                    mask, workspace, err)
     check("focus_window_attn", lib().focus_window_attn(C.byref(d), _stream(stream, q.device)))

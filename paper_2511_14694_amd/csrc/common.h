@@ -26,6 +26,15 @@ inline focus_status launch_status() {
 // Number of XCDs (each with its own L2) blocks are dealt over, round robin.
 constexpr int kXcds = 8;
 
+// Compute units of the current device (256 if the query fails).
+inline int device_cus() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    return 256;
+  return cus;
+}
+
 // --------------------------------------------------------------- device side
 
 __device__ inline void raise_err(int32_t* err, int32_t bit) {

@@ -231,21 +231,13 @@ __global__ __launch_bounds__(D) void decode_combine(focus_decode_desc d, int spl
   if (e == 0 && h == 0 && (d.kind[b] & FOCUS_STEP_WINDOW_END)) d.win_len[b] = 0;
 }
 
-int device_cus() {
-  int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
-    return 256;
-  return cus;
-}
-
 int auto_split(int64_t batch, int64_t cap) {
   // About 7/8 as many workgroups as compute units for a full cache: a single
   // round of long-running workgroups.  Once the count passes the CU count, a
   // partial second round leaves most CUs idle at the end (batch 16 x 11 000
   // keys on 256 CUs: 272 workgroups read 56 % of HBM bandwidth, 208-240 read
   // 71-75 %, 704 read 68 %).
-  const int64_t target = std::max(1, device_cus() * 7 / 8);
+  const int64_t target = std::max(1, focus::device_cus() * 7 / 8);
   int64_t s = focus::ceil_div(batch * cap, target);
   s = focus::ceil_div(s, 16) * 16;
   return (int)(s < 16 ? 16 : s > (1 << 30) ? (1 << 30) : s);

@@ -154,13 +154,28 @@ struct SumQ {
   int64_t base, rows;
 };
 
+// Key split (C(t), bf16): when a launch has fewer workgroups than the device
+// has compute units (one window per call), each (window, head, query tile)
+// item is split into n workgroups over consecutive ranges of its key tiles.
+// Each writes its rows' unnormalised float32 output and (running max, sum) in
+// the exp2 domain to the workspace, [split][listed window][row][head][D] and
+// [split][listed window][row][head][2]; attn_combine merges them.
+struct Split {
+  int n;        // 1 = no split
+  float* po;    // partial outputs
+  float* pml;   // (max, sum) pairs
+  int64_t rows; // rows per listed window in the workspace (max window tokens)
+  int64_t nwl;  // listed windows
+};
+constexpr Split kNoSplit = {1, nullptr, nullptr, 0, 0};
+
 // Under C(t) the workgroup has one more wave, which only copies tiles.
 template <bool KL, bool SQ>
 constexpr int producer_waves() { return (!KL && !SQ) ? 1 : 0; }
 
 template <int D, int W, bool KL, bool SQ>
 __global__ __launch_bounds__(64 * (W + producer_waves<KL, SQ>()), (W == 1 || producer_waves<KL, SQ>()) ? 1 : 2) void attn_bf16(
-    focus_attn_desc d, float sc, int64_t n_pairs, int QT, SumQ sq) {
+    focus_attn_desc d, float sc, int64_t n_pairs, int QT, SumQ sq, Split sp) {
   using C = Cfg<D, W>;
   // Two K and two V tile buffers as separate arrays, referenced statically by
   // a loop unrolled by two: the compiler can then tell a tile being read from
@@ -175,7 +190,15 @@ __global__ __launch_bounds__(64 * (W + producer_waves<KL, SQ>()), (W == 1 || pro
   __shared__ __attribute__((aligned(1024))) char vbuf2[kStages == 3 ? C::kTile : 16];
 
   const int tid = threadIdx.x;
-  const Item it = map_block(blockIdx.x, n_pairs, d.n_heads, QT);
+  // Split: the n workgroups of an item are consecutive blocks of one XCD.
+  int64_t bid = blockIdx.x;
+  int split = 0;
+  if (sp.n > 1) {
+    const int64_t r = bid / focus::kXcds;
+    split = (int)(r % sp.n);
+    bid = (r / sp.n) * focus::kXcds + bid % focus::kXcds;
+  }
+  const Item it = map_block(bid, n_pairs, d.n_heads, QT);
   if (!it.valid) return;
   const int64_t gw = listed_window(d, it.list_idx);
   if (gw < 0 || gw >= d.totals.n_windows) {
@@ -231,7 +254,9 @@ __global__ __launch_bounds__(64 * (W + producer_waves<KL, SQ>()), (W == 1 || pro
   }
   const int nct = KL ? (nsum + C::kBK) / C::kBK : (Cw + C::kBK - 1) / C::kBK;
   const int nwt = (nwk + C::kBK - 1) / C::kBK - tw0;
-  const int ntiles = nct + nwt;
+  // This workgroup's tiles [tb, tb + ntiles) of the item's nct + nwt.
+  const int tb = (int)((int64_t)split * (nct + nwt) / sp.n);
+  const int ntiles = (int)((int64_t)(split + 1) * (nct + nwt) / sp.n) - tb;
 
   const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, g = lane >> 5;
   const int js = q0 + wave * 32 + l32;  // this lane's query slot
@@ -452,6 +477,7 @@ __global__ __launch_bounds__(64 * (W + producer_waves<KL, SQ>()), (W == 1 || pro
 
   if constexpr (kStages == 2) {
     // The barrier closing each step also waits for the next tile's copies.
+    // (These modes are never split: tb = 0.)
     issue_tile(0, kbuf0, vbuf0);
     __syncthreads();
     for (int t = 0; t < ntiles; t += 2) {
@@ -506,12 +532,14 @@ __global__ __launch_bounds__(64 * (W + producer_waves<KL, SQ>()), (W == 1 || pro
           __builtin_amdgcn_global_load_lds(vs, (lds_void*)(vbuf + i * 1024), 16, 0, 0);
         }
       };
-      copy_tile(0, kbuf0, vbuf0);
-      copy_tile(min(1, ntiles - 1), kbuf1, vbuf1);
+      if (ntiles > 0) {
+        copy_tile(tb, kbuf0, vbuf0);
+        copy_tile(tb + min(1, ntiles - 1), kbuf1, vbuf1);
+      }
       __syncthreads();  // tiles 0 and 1 have landed
       for (int t = 0; t < ntiles; ++t) {
         const int nb = (t + 2) % 3;
-        copy_tile(min(t + 2, ntiles - 1), nb == 0 ? kbuf0 : nb == 1 ? kbuf1 : kbuf2,
+        copy_tile(tb + min(t + 2, ntiles - 1), nb == 0 ? kbuf0 : nb == 1 ? kbuf1 : kbuf2,
                   nb == 0 ? vbuf0 : nb == 1 ? vbuf1 : vbuf2);
         end_step(true);
       }
@@ -520,18 +548,33 @@ __global__ __launch_bounds__(64 * (W + producer_waves<KL, SQ>()), (W == 1 || pro
     }
     __syncthreads();
     for (int t = 0; t < ntiles; t += 3) {
-      compute_tile(t, kbuf0, vbuf0);
+      compute_tile(tb + t, kbuf0, vbuf0);
       end_step(false);
       if (t + 1 >= ntiles) break;
-      compute_tile(t + 1, kbuf1, vbuf1);
+      compute_tile(tb + t + 1, kbuf1, vbuf1);
       end_step(false);
       if (t + 2 >= ntiles) break;
-      compute_tile(t + 2, kbuf2, vbuf2);
+      compute_tile(tb + t + 2, kbuf2, vbuf2);
       end_step(false);
     }
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
+  if (sp.n > 1) {
+    // key split: the unnormalised output and (max, sum) of this tile range
+    if (qi < T && qi < sp.rows) {
+      const int64_t pidx = (((int64_t)split * sp.nwl + it.list_idx) * sp.rows + qi) * H + h;
+      float* op = sp.po + pidx * D;
+#pragma unroll
+      for (int dt = 0; dt < C::kDtiles; ++dt)
+#pragma unroll
+        for (int v4 = 0; v4 < 4; ++v4)
+          *reinterpret_cast<float4*>(op + 32 * dt + 8 * v4 + 4 * g) =
+              make_float4(oacc[dt][4 * v4], oacc[dt][4 * v4 + 1], oacc[dt][4 * v4 + 2], oacc[dt][4 * v4 + 3]);
+      if (g == 0) *reinterpret_cast<float2*>(sp.pml + pidx * 2) = make_float2(m_run, l_tot);
+    }
+    return;
+  }
   if (SQ ? js < nq : qi < T) {
     const float inv = 1.f / l_tot;
     const int64_t orow = SQ ? s0 + js - sq.base : tok0 + qi;
@@ -811,6 +854,56 @@ __global__ __launch_bounds__(64) void attn_sq_group(focus_attn_desc d, float sc,
   }
 }
 
+// ------------------------------------------------- bf16 key-split merge
+
+// Merges the key-split partials of every (listed window, row, head): with
+// M = max_s m_s and w_s = 2^(m_s - M), O = sum_s w_s o_s / sum_s w_s l_s and
+// LSE = (M + log2 sum_s w_s l_s) ln 2 (m, l in the exp2 domain, as the split
+// workgroups left them).  D / 4 lanes per (row, head), four outputs each; the
+// windows the attention kernel skipped (rows outside the buffers) are skipped
+// here too.
+template <int D>
+__global__ __launch_bounds__(256) void attn_combine(focus_attn_desc d, Split sp) {
+  constexpr int kL = D / 4;
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t item = gid / kL;
+  const int c = (int)(gid % kL);
+  const int H = d.n_heads;
+  const int64_t li = item / (sp.rows * H);
+  if (li >= sp.nwl) return;
+  const int qi = (int)(item / H % sp.rows), h = (int)(item % H);
+  const int64_t gw = listed_window(d, li);
+  if (gw < 0 || gw >= d.totals.n_windows) return;
+  const int T = d.win_ntok[gw];
+  const int Cw = d.win_cache_off[gw];
+  const int b = d.win_seq[gw];
+  const int64_t tok0 = d.win_tok_off[gw] - d.qkv_tok_base;
+  if (qi >= T || b < 0 || b >= d.batch || Cw < 0 || Cw > d.cache_cap || tok0 < 0 || tok0 + T > d.qkv_rows) return;
+  const int64_t stride = sp.nwl * sp.rows * H;  // (row, head) entries per split
+  const int64_t p0 = (li * sp.rows + qi) * H + h;
+  float mx = kMinit;
+  for (int s = 0; s < sp.n; ++s) mx = fmaxf(mx, sp.pml[2 * (p0 + s * stride)]);
+  float l = 0.f;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int s = 0; s < sp.n; ++s) {
+    const int64_t p = p0 + s * stride;
+    const float w = __builtin_amdgcn_exp2f(sp.pml[2 * p] - mx);
+    l += w * sp.pml[2 * p + 1];
+    const float4 o = *reinterpret_cast<const float4*>(sp.po + p * D + 4 * c);
+    acc.x += w * o.x;
+    acc.y += w * o.y;
+    acc.z += w * o.z;
+    acc.w += w * o.w;
+  }
+  const float inv = 1.f / l;
+  uint2 out;
+  out.x = focus::pack_bf16x2(acc.x * inv, acc.y * inv);
+  out.y = focus::pack_bf16x2(acc.z * inv, acc.w * inv);
+  const int64_t orow = tok0 + qi;
+  *reinterpret_cast<uint2*>(reinterpret_cast<__bf16*>(d.o) + (orow * H + h) * D + 4 * c) = out;
+  if (c == 0 && d.lse) d.lse[orow * H + h] = (mx + log2f(l)) * kLn2;
+}
+
 // ----------------------------------------------------------------- f32 VALU
 
 template <int D, bool KL>
@@ -932,11 +1025,40 @@ __global__ __launch_bounds__(256) void attn_f32(focus_attn_desc d, float sc, int
   }
 }
 
+// Query tile rows of a launch: 32 per computing wave (bf16), 64 (f32).
+int attn_rows_per_tile(const focus_attn_desc* d) {
+  return d->dtype == FOCUS_BF16 ? 32 * (d->mask == FOCUS_MASK_KMER_LOCAL ? kBf16WavesKL : kBf16Waves) : 64;
+}
+
+// Key splits of a C(t) bf16 launch (1 = none): as many as still fit the
+// (window, head, query tile) items in one round of workgroups, one per CU,
+// at most 16 and with at least 8 key tiles per split.
+int attn_split_count(const focus_attn_desc* d) {
+  if (d->dtype != FOCUS_BF16 || d->mask != FOCUS_MASK_CT || d->n_heads <= 0) return 1;
+  const focus_layout_totals& t = d->totals;
+  const int64_t nwl = d->win_ids ? d->n_win : t.n_windows;
+  if (nwl <= 0 || t.max_window_tokens <= 0 || t.max_window_cache < 0) return 1;
+  const int64_t items = nwl * d->n_heads * focus::ceil_div(t.max_window_tokens, attn_rows_per_tile(d));
+  const int64_t tiles = focus::ceil_div(t.max_window_cache, 64) + focus::ceil_div(t.max_window_tokens, 64);
+  int64_t n = focus::device_cus() / items;
+  n = n < tiles / 8 ? n : tiles / 8;
+  n = n < 16 ? n : 16;
+  return n < 2 ? 1 : (int)n;
+}
+
+size_t attn_split_bytes(const focus_attn_desc* d, int n) {
+  if (n < 2) return 0;
+  const focus_layout_totals& t = d->totals;
+  const int64_t nwl = d->win_ids ? d->n_win : t.n_windows;
+  const int64_t rows = focus::ceil_div(t.max_window_tokens, attn_rows_per_tile(d)) * attn_rows_per_tile(d);
+  return (size_t)n * nwl * rows * d->n_heads * (d->head_dim + 2) * sizeof(float);
+}
+
 }  // namespace
 
 extern "C" size_t focus_window_attn_workspace(const focus_attn_desc* d) {
-  (void)d;
-  return 0;
+  if (!d) return 0;
+  return attn_split_bytes(d, attn_split_count(d));
 }
 
 extern "C" focus_status focus_window_attn(const focus_attn_desc* d, focus_stream_t stream) {
@@ -962,36 +1084,57 @@ extern "C" focus_status focus_window_attn(const focus_attn_desc* d, focus_stream
       (reinterpret_cast<uintptr_t>(d->lse) & 3u))
     return FOCUS_E_ARG;
   if (!d->win_ids && t.max_window_cache > d->cache_cap) return FOCUS_E_CAPACITY;
-  if (focus_window_attn_workspace(d) > d->workspace_bytes) return FOCUS_E_WORKSPACE;
 
   const float scale = d->softmax_scale > 0.f ? d->softmax_scale : 1.0f / sqrtf((float)d->head_dim);
   const float sc = scale * kLog2e;
   const int64_t n_pairs = nwl * d->n_heads;
   const bool kl = d->mask == FOCUS_MASK_KMER_LOCAL;
   const int waves = kl ? kBf16WavesKL : kBf16Waves;
-  const int bq = d->dtype == FOCUS_BF16 ? 32 * waves : 64;
+  const int bq = attn_rows_per_tile(d);
   // (C(t): one more wave, which copies the tiles)
   const int threads = d->dtype == FOCUS_BF16 ? 64 * (waves + (kl ? 0 : 1)) : 256;
   const int64_t qt = focus::ceil_div(t.max_window_tokens, bq);
-  const int64_t blocks = focus::ceil_div(n_pairs, focus::kXcds) * focus::kXcds * qt;
+  // Key split when the workspace allows it (else one workgroup per item).
+  Split sp = kNoSplit;
+  const int n_split = attn_split_count(d);
+  const size_t split_bytes = attn_split_bytes(d, n_split);
+  if (n_split > 1 && d->workspace && focus::aligned16(d->workspace) && d->workspace_bytes >= split_bytes) {
+    sp.n = n_split;
+    sp.rows = qt * bq;
+    sp.nwl = nwl;
+    sp.po = reinterpret_cast<float*>(d->workspace);
+    sp.pml = sp.po + (int64_t)n_split * nwl * sp.rows * d->n_heads * d->head_dim;
+  }
+  const int64_t blocks = focus::ceil_div(n_pairs, focus::kXcds) * focus::kXcds * qt * sp.n;
   if (blocks * threads >= ((int64_t)1 << 32) || qt > INT32_MAX) return FOCUS_E_SHAPE;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const dim3 grid((uint32_t)blocks), block(threads);
-#define FOCUS_ATTN_LAUNCH(KERNEL) hipLaunchKernelGGL(KERNEL, grid, block, 0, s, *d, sc, n_pairs, (int)qt, SumQ{})
+#define FOCUS_ATTN_LAUNCH(KERNEL) hipLaunchKernelGGL(KERNEL, grid, block, 0, s, *d, sc, n_pairs, (int)qt, SumQ{}, sp)
+#define FOCUS_F32_LAUNCH(KERNEL) hipLaunchKernelGGL(KERNEL, grid, block, 0, s, *d, sc, n_pairs, (int)qt, SumQ{})
   if (d->dtype == FOCUS_BF16) {
     if (d->head_dim == 128) {
       if (kl) FOCUS_ATTN_LAUNCH((attn_bf16<128, kBf16WavesKL, true, false>)); else FOCUS_ATTN_LAUNCH((attn_bf16<128, kBf16Waves, false, false>));
     } else {
       if (kl) FOCUS_ATTN_LAUNCH((attn_bf16<64, kBf16WavesKL, true, false>)); else FOCUS_ATTN_LAUNCH((attn_bf16<64, kBf16Waves, false, false>));
     }
+    if (sp.n > 1) {
+      const int64_t lanes = sp.nwl * sp.rows * d->n_heads * (d->head_dim / 4);
+      const int64_t cblocks = focus::ceil_div(lanes, 256);
+      if (cblocks > INT32_MAX) return FOCUS_E_SHAPE;
+      if (d->head_dim == 128)
+        hipLaunchKernelGGL((attn_combine<128>), dim3((uint32_t)cblocks), dim3(256), 0, s, *d, sp);
+      else
+        hipLaunchKernelGGL((attn_combine<64>), dim3((uint32_t)cblocks), dim3(256), 0, s, *d, sp);
+    }
   } else {
     if (d->head_dim == 128) {
-      if (kl) FOCUS_ATTN_LAUNCH((attn_f32<128, true>)); else FOCUS_ATTN_LAUNCH((attn_f32<128, false>));
+      if (kl) FOCUS_F32_LAUNCH((attn_f32<128, true>)); else FOCUS_F32_LAUNCH((attn_f32<128, false>));
     } else {
-      if (kl) FOCUS_ATTN_LAUNCH((attn_f32<64, true>)); else FOCUS_ATTN_LAUNCH((attn_f32<64, false>));
+      if (kl) FOCUS_F32_LAUNCH((attn_f32<64, true>)); else FOCUS_F32_LAUNCH((attn_f32<64, false>));
     }
   }
 #undef FOCUS_ATTN_LAUNCH
+#undef FOCUS_F32_LAUNCH
   return focus::launch_status();
 }
 
@@ -1071,7 +1214,7 @@ extern "C" focus_status focus_adapter_attn(const focus_adapter_desc* a, focus_st
   const int64_t blocks = focus::ceil_div(n_pairs, focus::kXcds) * focus::kXcds * qt;
   if (blocks * 64 >= ((int64_t)1 << 32) || qt > INT32_MAX) return FOCUS_E_SHAPE;
   const dim3 grid((uint32_t)blocks), block(64);
-#define FOCUS_SQ_LAUNCH(KERNEL) hipLaunchKernelGGL(KERNEL, grid, block, 0, s, d, sc, n_pairs, (int)qt, sq)
+#define FOCUS_SQ_LAUNCH(KERNEL) hipLaunchKernelGGL(KERNEL, grid, block, 0, s, d, sc, n_pairs, (int)qt, sq, kNoSplit)
   if (a->head_dim == 128) {
     if (kl) FOCUS_SQ_LAUNCH((attn_bf16<128, 1, true, true>)); else FOCUS_SQ_LAUNCH((attn_bf16<128, 1, false, true>));
   } else {

@@ -6,8 +6,11 @@ sequences); the workloads at full size run the very launch the benchmark times
 (every window of every sequence in one masked-parallel launch) and compare
 sampled windows and heads; the dense 32 kb point compares sampled rows.
 Properties checked on the device output: streaming (one window per call, the
-cache filled as it goes) equals masked-parallel bit for bit, two runs are
-bitwise equal, every softmax row sums to one through the returned LSE.
+cache filled as it goes) equals masked-parallel bit for bit when neither splits
+keys, two runs are bitwise equal, every softmax row sums to one through the
+returned LSE.  Launches with few (window, head, query tile) items split each
+item's keys over several workgroups (merged by log-sum-exp): those are checked
+against the oracle directly, including splits left without a key tile.
 """
 
 import numpy as np
@@ -138,14 +141,19 @@ def test_custom_scale():
     compare_windows(ref, p, range(3), [0, 1], "scale 0.3")
 
 
+def _no_split():
+    return torch.empty(0, dtype=torch.uint8, device=DEV)
+
+
 def test_streaming_equals_masked_parallel_bitwise():
     """One window per call, in order, compacting each window right after its
     attention and passing only the window's rows, reproduces the single
-    masked-parallel launch bit for bit."""
+    masked-parallel launch bit for bit (both without the key split)."""
     announce("attn streaming vs masked-parallel")
     seq, W = [3000, 1200], 500
     km = _kmer_for(seq, W, None, 3)
-    p = Prefill(seq, W, km, 4, 2, 128, "bf16", seed=5)
+    p = Prefill(seq, W, km, 4, 2, 128, "bf16", seed=5, run=False)
+    p.o, p.lse = p.attn(workspace=_no_split())
     ref = build_layout(seq, W, km)
     ck = torch.zeros_like(p.ck)
     cv = torch.zeros_like(p.cv)
@@ -156,13 +164,41 @@ def test_streaming_equals_masked_parallel_bitwise():
         ids = torch.tensor([w], dtype=torch.int32, device=DEV)
         sl = slice(t0, t0 + T)
         ow, lw = F.focus_window_attn(p.lay, p.q[sl].contiguous(), p.k[sl].contiguous(), p.v[sl].contiguous(),
-                                     ck, cv, win_ids=ids, qkv_tok_base=t0, err=p.err)
+                                     ck, cv, win_ids=ids, qkv_tok_base=t0, err=p.err, workspace=_no_split())
         o[sl], lse[sl] = ow, lw
         F.focus_compact_kv(p.lay, p.k[sl].contiguous(), p.v[sl].contiguous(), ck, cv, win_ids=ids,
                            kv_tok_base=t0, err=p.err)
     torch.cuda.synchronize()
     assert int(p.err.item()) == 0
     assert torch.equal(o, p.o) and torch.equal(lse, p.lse)
+
+
+@pytest.mark.parametrize("seq,H,Hkv,D,wins", [
+    ([300_000], 2, 1, 128, [299, 0]),   # 7 splits; window 0's first tile: 4 key tiles
+    ([100_000], 4, 2, 64, [99]),        # 4 splits, head_dim 64
+])
+def test_key_split_against_oracle(seq, H, Hkv, D, wins):
+    """Few items per launch: each item's key tiles are split over several
+    workgroups and merged; every row of the listed windows against the
+    oracle, and against the unsplit launch to float32 rounding."""
+    announce(f"attn key split seq={seq} H={H}/{Hkv} D={D} windows={wins}")
+    W = 1000
+    km = np.full(-(-seq[0] // W), 100, np.int32)
+    p = Prefill(seq, W, km, H, Hkv, D, "bf16", seed=31, run=False)
+    ids = torch.tensor(wins, dtype=torch.int32, device=DEV)
+    assert F.focus_window_attn_workspace(p.lay, p.q, p.k, p.v, p.ck, p.cv, ids) > 0
+    p.o, p.lse = p.attn(win_ids=ids)
+    ref = build_layout(seq, W, km)
+    compare_windows(ref, p, wins, list(range(H)), "key split")
+    o1, lse1 = p.attn(win_ids=ids, workspace=_no_split())
+    for w in wins:
+        sl = slice(int(ref["win_tok_off"][w]), int(ref["win_tok_off"][w] + ref["win_ntok"][w]))
+        assert (p.o[sl].float() - o1[sl].float()).abs().max().item() < 2e-2
+        assert (p.lse[sl] - lse1[sl]).abs().max().item() < 1e-4
+    o2, lse2 = p.attn(win_ids=ids)
+    for w in wins:  # deterministic (rows of unlisted windows are not written)
+        sl = slice(int(ref["win_tok_off"][w]), int(ref["win_tok_off"][w] + ref["win_ntok"][w]))
+        assert torch.equal(o2[sl], p.o[sl]) and torch.equal(lse2[sl], p.lse[sl])
 
 
 def test_window_subset_any_order_and_determinism():
@@ -246,6 +282,14 @@ def test_workload_full_size_sampled(name):
     heads = [0, 13, w.heads - 1]
     worst = compare_windows(ref, p, _sample_windows(ref, w.index), heads, name)
     print(f"[parity] {name}: worst max-abs {worst[0]:.3e} rel-L2 {worst[1]:.3e}", flush=True)
+    if name == "prefill_1mb":
+        # the streaming launch the benchmark times: one window per call (key split)
+        last = ref["n_windows"] - 1
+        ids = torch.tensor([last], dtype=torch.int32, device=DEV)
+        assert F.focus_window_attn_workspace(p.lay, p.q, p.k, p.v, p.ck, p.cv, ids) > 0
+        p.attn(win_ids=ids, o=p.o, lse=p.lse)
+        e = compare_windows(ref, p, [last], heads, f"{name} streaming")
+        print(f"[parity] {name} streaming: max-abs {e[0]:.3e} rel-L2 {e[1]:.3e}", flush=True)
     del p
     torch.cuda.empty_cache()
 
