@@ -223,6 +223,33 @@ def secondary_compaction(torch, F, s, timer, reps=10):
             "GBps": nbytes / ms / 1e6, "frac_hbm": nbytes / (ms * 1e-3) / PEAK_HBM}
 
 
+def secondary_hbm_reference(torch, nbytes=4 << 30, reps=10):
+    """What plain PyTorch device ops reach on this machine's HBM (context for the
+    HBM-bound kernels' fractions; not part of the hot path): a row-wise max
+    over 4 GiB (read), a fill (write) and a copy (read + write)."""
+    x = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda:0").normal_()
+    y = torch.empty_like(x)
+
+    def t(f):
+        f()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            f()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    read = nbytes / (t(lambda: torch.amax(x.view(-1, 4096), dim=1)) * 1e-3)
+    write = nbytes / (t(lambda: y.fill_(1.0)) * 1e-3)
+    copy = 2 * nbytes / (t(lambda: y.copy_(x)) * 1e-3)
+    del x, y
+    torch.cuda.empty_cache()
+    return {"read_GBps": read / 1e9, "write_GBps": write / 1e9, "copy_GBps": copy / 1e9,
+            "note": "torch.amax over rows (read), fill_ (write), copy_ (read + write) of 4 GiB"}
+
+
 def secondary_decode(torch, F, fw, steps=None):
     """Batch-16 decode at ~1 Mb: 10 000 cached summaries plus a partial window."""
     from paper_2511_14694_amd import schedule
@@ -558,6 +585,8 @@ def main():
     if not args.no_secondary:
         log("secondary: compaction")
         sec = {"compaction_1mb": secondary_compaction(torch, F, s, timer)}
+        log("secondary: HBM reference")
+        sec["hbm_reference"] = secondary_hbm_reference(torch)
         log("secondary: streaming")
         sec["streaming_1mb"] = secondary_streaming(torch, F, s)
         log("secondary: k-mer-local mask")
