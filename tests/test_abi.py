@@ -229,3 +229,31 @@ def test_fidelity_host_validation(mutate, status):
     d = _fid_ok()
     mutate(d)
     assert _call("focus_fidelity", d) == status
+
+
+def test_window_attn_workspace_key_split_formula():
+    """Key split of a bf16 C(t) launch: n = min(CUs // items, key tiles // 8, 16)
+    splits when that is at least 2, each holding float32 (O, max, sum) per
+    (listed window, padded row, head); otherwise no workspace.  (MI355X: 256
+    CUs, also the fallback when no device answers.)"""
+    d = _attn_ok()
+    d.totals = F.focus_layout_plan([1_000_000], 1000, None, 100)
+    d.n_heads = d.n_kv_heads = 32
+    t = d.totals
+    assert (t.max_window_tokens, t.max_window_cache) == (1010, 9990)
+    ws = lambda: _abi.lib().focus_window_attn_workspace(C.byref(d))
+    assert ws() == 0                                   # every window: 128 000 items
+    d.win_ids, d.n_win = 1 << 20, 1                    # one window: 32 heads x 4 query tiles
+    rows = 4 * 256
+    assert ws() == 2 * 1 * rows * 32 * (128 + 2) * 4   # 256 // 128 = 2 splits
+    d.n_heads = d.n_kv_heads = 4                       # 16 items: 16 splits (173 tiles // 8 = 21)
+    assert ws() == 16 * 1 * rows * 4 * (128 + 2) * 4
+    d.head_dim = 64
+    assert ws() == 16 * 1 * rows * 4 * (64 + 2) * 4
+    d.mask = 1
+    assert ws() == 0                                   # k-mer-local: never split
+    d.mask, d.dtype = 0, 1
+    assert ws() == 0                                   # float32: never split
+    d.dtype = 0
+    d.totals = F.focus_layout_plan([100], 50, None, 10)
+    assert ws() == 0                                   # two key tiles: nothing to split
