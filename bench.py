@@ -576,7 +576,7 @@ def main():
         "roofline": {"bound": "mfma", "achieved": flops / (attn_ms * 1e-3) / 1e12,
                      "peak": PEAK_BF16_FLOPS / 1e12, "unit": "TFLOP/s",
                      "frac": flops / (attn_ms * 1e-3) / PEAK_BF16_FLOPS, "traffic": traffic,
-                     "kernel": "attn_bf16<128> (focus_window_attn)", "flops_per_launch": flops,
+                     "kernel": "attn_ct<128> (focus_window_attn)", "flops_per_launch": flops,
                      "avg_launch_ms": attn_ms},
         "kernel_ms": {"layout": timer.mean_ms("layout"), "compact": timer.mean_ms("compact"),
                       "attn": attn_ms},

@@ -33,6 +33,12 @@ HIPCC_FLAGS = [
 ]
 
 
+# Per-source extra flags.  The attention kernels never see a NaN (finite
+# inputs; masked scores are -inf), so their max reductions need no NaN
+# canonicalisation.
+EXTRA_FLAGS = {"window_attn.hip": ["-fno-honor-nans"]}
+
+
 def _hipcc() -> str:
     for cand in (os.environ.get("HIPCC"), shutil.which("hipcc"), "/opt/rocm/bin/hipcc"):
         if cand and os.path.exists(cand):
@@ -62,7 +68,7 @@ def build(verbose: bool = False, save_temps: bool = False) -> str:
         for src in SOURCES:
             obj = os.path.join(BUILD, src.replace(".hip", ".o"))
             objs.append(obj)
-            cmd = [hipcc, *HIPCC_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+            cmd = [hipcc, *HIPCC_FLAGS, *EXTRA_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
             if save_temps:
                 cmd.insert(1, "-save-temps=obj")
             jobs.append(ex.submit(_run, cmd, verbose))

@@ -14,14 +14,15 @@
 // then only the window tiles that hold the block's k-mers; a two-sided mask
 // keeps each row's own k-mer.
 //
-// bf16 path (the hot one): one workgroup = 8 waves (4 under the k-mer-local
-// mask) = 32 query rows per wave of one (window, head); keys stream in tiles
-// of 64 through LDS, copied global -> LDS directly (under C(t) three buffers
-// and a ninth wave that does all the copying; otherwise two buffers, each wave
-// copying its share):
+// bf16 path under C(t) (the hot one, attn_ct): one workgroup = 8 waves x 32
+// query rows of one (window, head), two waves per SIMD; keys arrive in 64-key
+// tiles copied global -> LDS directly through four LDS stages, and each wave
+// runs a one-sub-tile (32 keys) software pipeline:
 //   S^T = K Q^T   v_mfma_f32_32x32x16_bf16: each lane ends up holding one
 //                 query's scores for 16 keys of a 32-key block, so the row
 //                 max / row sum are lane-local plus one exchange with lane^32;
+//                 the next sub-tile's scores are issued on the MFMA pipe while
+//                 the VALU does this sub-tile's softmax;
 //   softmax       exp2 domain, running max with lazy rescaling: the output
 //                 accumulator is rescaled only when a row's max grows by more
 //                 than 2^8, which keeps exp2 arguments <= 8 and is exact;
@@ -33,6 +34,9 @@
 // (window, head) land on the same XCD (sharing K/V through its L2) and the
 // listed windows are started in list order (last window = largest cache first
 // by default).
+//
+// The k-mer-local mask (attn_bf16<D, 4, true, false>) keeps the simpler
+// two-stage form of the same MFMA scheme: 4 waves, each copying its share.
 //
 // Summary queries (the FOCUS adapter's attention): under C(t) several windows'
 // summaries share one wave (attn_sq_group); otherwise the bf16 kernel above
@@ -169,36 +173,21 @@ struct Split {
 };
 constexpr Split kNoSplit = {1, nullptr, nullptr, 0, 0};
 
-// Under C(t) the workgroup has one more wave, which only copies tiles.
-template <bool KL, bool SQ>
-constexpr int producer_waves() { return (!KL && !SQ) ? 1 : 0; }
-
+// The k-mer-local and summary-query modes (the C(t) window attention is
+// attn_ct below).
 template <int D, int W, bool KL, bool SQ>
-__global__ __launch_bounds__(64 * (W + producer_waves<KL, SQ>()), (W == 1 || producer_waves<KL, SQ>()) ? 1 : 2) void attn_bf16(
-    focus_attn_desc d, float sc, int64_t n_pairs, int QT, SumQ sq, Split sp) {
+__global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_desc d, float sc, int64_t n_pairs,
+                                                                     int QT, SumQ sq) {
+  static_assert(KL || SQ, "C(t) window attention is attn_ct");
   using C = Cfg<D, W>;
   // Two K and two V tile buffers as separate arrays, referenced statically by
   // a loop unrolled by two: the compiler can then tell a tile being read from
   // the one being filled, and waits for the copies only at the barrier.
-  // Under C(t) a third K and V buffer lets copies run two steps ahead (one
-  // workgroup per CU: the register budget allows no second, so the LDS is
-  // there); the k-mer-local and summary-query modes keep two.
-  constexpr int kStages = (!KL && !SQ) ? 3 : 2;
   __shared__ __attribute__((aligned(1024))) char kbuf0[C::kTile], kbuf1[C::kTile];
   __shared__ __attribute__((aligned(1024))) char vbuf0[C::kTile], vbuf1[C::kTile];
-  __shared__ __attribute__((aligned(1024))) char kbuf2[kStages == 3 ? C::kTile : 16];
-  __shared__ __attribute__((aligned(1024))) char vbuf2[kStages == 3 ? C::kTile : 16];
 
   const int tid = threadIdx.x;
-  // Split: the n workgroups of an item are consecutive blocks of one XCD.
-  int64_t bid = blockIdx.x;
-  int split = 0;
-  if (sp.n > 1) {
-    const int64_t r = bid / focus::kXcds;
-    split = (int)(r % sp.n);
-    bid = (r / sp.n) * focus::kXcds + bid % focus::kXcds;
-  }
-  const Item it = map_block(bid, n_pairs, d.n_heads, QT);
+  const Item it = map_block(blockIdx.x, n_pairs, d.n_heads, QT);
   if (!it.valid) return;
   const int64_t gw = listed_window(d, it.list_idx);
   if (gw < 0 || gw >= d.totals.n_windows) {
@@ -255,8 +244,7 @@ __global__ __launch_bounds__(64 * (W + producer_waves<KL, SQ>()), (W == 1 || pro
   const int nct = KL ? (nsum + C::kBK) / C::kBK : (Cw + C::kBK - 1) / C::kBK;
   const int nwt = (nwk + C::kBK - 1) / C::kBK - tw0;
   // This workgroup's tiles [tb, tb + ntiles) of the item's nct + nwt.
-  const int tb = (int)((int64_t)split * (nct + nwt) / sp.n);
-  const int ntiles = (int)((int64_t)(split + 1) * (nct + nwt) / sp.n) - tb;
+  const int ntiles = nct + nwt;
 
   const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, g = lane >> 5;
   const int js = q0 + wave * 32 + l32;  // this lane's query slot
@@ -475,9 +463,8 @@ __global__ __launch_bounds__(64 * (W + producer_waves<KL, SQ>()), (W == 1 || pro
     }
   };
 
-  if constexpr (kStages == 2) {
+  {
     // The barrier closing each step also waits for the next tile's copies.
-    // (These modes are never split: tb = 0.)
     issue_tile(0, kbuf0, vbuf0);
     __syncthreads();
     for (int t = 0; t < ntiles; t += 2) {
@@ -489,74 +476,396 @@ __global__ __launch_bounds__(64 * (W + producer_waves<KL, SQ>()), (W == 1 || pro
       compute_tile(t + 1, kbuf1, vbuf1);
       __syncthreads();
     }
-  } else {
-    // Tile t lives in buffers t % 3.  The extra wave (wave W) does all the
-    // copying: step t starts the copies of tile t + 2 (into the buffers tile
-    // t - 1 left; past the last tile it copies the last tile again, into a
-    // buffer no later step reads) and ends by waiting until only those are in
-    // flight (tile t + 1 has landed); the W computing waves never wait on a
-    // copy, and a barrier closes every step for all W + 1.  (A wave stalls
-    // while the address unit takes its copies, one 1 KB wave copy at a time:
-    // here that is the copying wave alone.)  The signal fences keep the
-    // compiler from moving memory accesses across the wait and barrier.
-    constexpr int kAll = kDma * W;  // wave copies per tile and tensor
-    auto end_step = [&](bool copying) {
-      constexpr int kVm = 2 * kAll;  // s_waitcnt vmcnt(kVm) expcnt(7) lgkmcnt(0)
-      __atomic_signal_fence(__ATOMIC_SEQ_CST);
-      if (copying)
-        __builtin_amdgcn_s_waitcnt((kVm & 15) | ((kVm >> 4) << 14) | (7 << 4) | (0 << 8));
-      else
-        __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4) | (0 << 8));  // lgkmcnt(0)
-      __builtin_amdgcn_s_barrier();
-      __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    };
-    if (wave == W) {
-      // all kAll wave copies of a tensor: rows i kRPK + lane / kCh16.  (This
-      // wave reads no LDS, so its buffers may be chosen at run time.)
-      auto copy_tile = [&](int t, char* kbuf, char* vbuf) {
-        const bool in_cache = t < nct;
-        const int row0 = in_cache ? t * C::kBK : (t - nct) * C::kBK;
-        const int nvalid = (in_cache ? Cw : nwk) - row0;
-        const char* kb = (in_cache ? kcache : kwin) + (int64_t)row0 * row_bytes;
-        const char* vb = (in_cache ? vcache : vwin) + (int64_t)row0 * row_bytes;
-        const uint32_t last = (uint32_t)(nvalid - 1) * row_bytes;
-        const int lr = lane / C::kCh16, p = lane % C::kCh16;
+  }
+
+  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  if (SQ ? js < nq : qi < T) {
+    const float inv = 1.f / l_tot;
+    const int64_t orow = SQ ? s0 + js - sq.base : tok0 + qi;
+    __bf16* op = reinterpret_cast<__bf16*>(SQ ? sq.o : d.o) + (orow * H + h) * D;
 #pragma unroll
-        for (int i = 0; i < kAll; ++i) {
-          const int r = i * kRPK + lr;
-          const int f = D == 128 ? (r & 3) : ((r >> 1) & 1);
-          const uint32_t rb = min((uint32_t)r * row_bytes, last);
-          const char* ks = kb + (rb + (uint32_t)((p ^ (r % C::kCh16)) * 16));
-          const char* vs = vb + (rb + (uint32_t)((((p >> 2) ^ f) * 4 + (p & 3)) * 16));
-          __builtin_amdgcn_global_load_lds(ks, (lds_void*)(kbuf + i * 1024), 16, 0, 0);
-          __builtin_amdgcn_global_load_lds(vs, (lds_void*)(vbuf + i * 1024), 16, 0, 0);
-        }
-      };
-      if (ntiles > 0) {
-        copy_tile(tb, kbuf0, vbuf0);
-        copy_tile(tb + min(1, ntiles - 1), kbuf1, vbuf1);
+    for (int dt = 0; dt < C::kDtiles; ++dt)
+#pragma unroll
+      for (int v4 = 0; v4 < 4; ++v4) {
+        // oacc[dt][4 v4 + e] = O[qi][32 dt + 8 v4 + 4 g + e]
+        uint2 w;
+        w.x = focus::pack_bf16x2(oacc[dt][4 * v4 + 0] * inv, oacc[dt][4 * v4 + 1] * inv);
+        w.y = focus::pack_bf16x2(oacc[dt][4 * v4 + 2] * inv, oacc[dt][4 * v4 + 3] * inv);
+        *reinterpret_cast<uint2*>(op + 32 * dt + 8 * v4 + 4 * g) = w;
       }
-      __syncthreads();  // tiles 0 and 1 have landed
-      for (int t = 0; t < ntiles; ++t) {
-        const int nb = (t + 2) % 3;
-        copy_tile(tb + min(t + 2, ntiles - 1), nb == 0 ? kbuf0 : nb == 1 ? kbuf1 : kbuf2,
-                  nb == 0 ? vbuf0 : nb == 1 ? vbuf1 : vbuf2);
-        end_step(true);
+    float* lse = SQ ? sq.lse : d.lse;
+    if (g == 0 && lse) lse[orow * H + h] = (m_run + log2f(l_tot)) * kLn2;
+  }
+}
+
+// ------------------------------------------- bf16 MFMA, C(t), pipelined waves
+
+// The C(t) window attention: one workgroup = 8 waves x 32 query rows of one
+// (window, head), two waves per SIMD (up to 256 registers each).  Keys arrive
+// in 64-key tiles through four LDS stages (copies issued by every wave, three
+// tiles ahead, spread over the step); each wave walks the keys in 32-key
+// sub-tiles with a one-sub-tile software pipeline:
+//   V^T operands of sub-tile j are read from LDS;
+//   S_{j+1} = K_{j+1} Q^T is issued on the MFMA pipe (its K operands were read
+//     one sub-tile earlier), and runs while the VALU does the softmax of S_j;
+//   the K operands of sub-tile j + 2 are read;
+//   O^T += V_j^T P_j^T.
+// So every LDS operand is read about one sub-tile before its MFMA, and the
+// exponentials of one sub-tile overlap the score MFMAs of the next.  A
+// barrier closes every 64-key step; at its end each wave waits only for the
+// copies of the tile the next step starts reading.
+template <int D>
+struct CtCfg {
+  static constexpr int kWaves = 8;
+  static constexpr int kBQ = 32 * kWaves;                // query rows per block
+  static constexpr int kBK = 64;                         // keys per LDS tile
+  static constexpr int kRB = D * 2;                      // bytes per row
+  static constexpr int kTile = kBK * kRB;                // bytes per tile per tensor
+  static constexpr int kCh16 = kRB / 16;                 // 16-byte chunks per row
+  static constexpr int kKsteps = D / 16;                 // MFMA k-steps of QK^T
+  static constexpr int kDtiles = D / 32;                 // 32-row blocks of O^T
+  static constexpr int kRPK = 1024 / kRB;                // tile rows per 1 KB wave copy
+  static constexpr int kDma = kTile / 1024 / kWaves;     // wave copies per tile, tensor and wave
+  static constexpr int kPerStep = 2 * kDma;              // copies a wave issues per step
+};
+
+template <int D>
+__global__ __launch_bounds__(512, 2) void attn_ct(
+    focus_attn_desc d, float sc, int64_t n_pairs, int QT, Split sp) {
+  using C = CtCfg<D>;
+  static_assert(C::kDma >= 1 && C::kTile % (1024 * C::kWaves) == 0, "tile must split into 1 KB wave loads");
+  // Four K and four V stages as separate arrays, every reference static (the
+  // step loop is unrolled four times): the compiler then tells the buffer a
+  // read uses from the ones being filled.
+  __shared__ __attribute__((aligned(1024))) char kb0[C::kTile], kb1[C::kTile], kb2[C::kTile], kb3[C::kTile];
+  __shared__ __attribute__((aligned(1024))) char vb0[C::kTile], vb1[C::kTile], vb2[C::kTile], vb3[C::kTile];
+
+  const int tid = threadIdx.x;
+  int64_t bid = blockIdx.x;
+  int split = 0;
+  if (sp.n > 1) {
+    const int64_t r = bid / focus::kXcds;
+    split = (int)(r % sp.n);
+    bid = (r / sp.n) * focus::kXcds + bid % focus::kXcds;
+  }
+  const Item it = map_block(bid, n_pairs, d.n_heads, QT);
+  if (!it.valid) return;
+  const int64_t gw = listed_window(d, it.list_idx);
+  if (gw < 0 || gw >= d.totals.n_windows) {
+    if (tid == 0 && it.qt == 0) focus::raise_err(d.err, FOCUS_ERR_BOUNDS);
+    return;
+  }
+  const int T = d.win_ntok[gw];
+  const int q0 = it.qt * C::kBQ;
+  if (q0 >= T) return;
+  const int Cw = d.win_cache_off[gw];
+  const int b = d.win_seq[gw];
+  const int64_t tok0 = d.win_tok_off[gw] - d.qkv_tok_base;
+  if (b < 0 || b >= d.batch || Cw < 0 || Cw > d.cache_cap || tok0 < 0 || tok0 + T > d.qkv_rows) {
+    if (tid == 0) focus::raise_err(d.err, FOCUS_ERR_BOUNDS);
+    return;
+  }
+  const int H = d.n_heads, Hkv = d.n_kv_heads, h = it.h;
+  const int hk = h / (H / Hkv);
+  const int nwk = min(T, q0 + C::kBQ);  // window keys any query of this block sees
+  // keys: nct tiles of cache rows [0, Cw), then nwt tiles of window rows [0, nwk)
+  const int nct = (Cw + C::kBK - 1) / C::kBK;
+  const int nwt = (nwk + C::kBK - 1) / C::kBK;
+  const int tb = (int)((int64_t)split * (nct + nwt) / sp.n);
+  const int ntiles = (int)((int64_t)(split + 1) * (nct + nwt) / sp.n) - tb;
+
+  // (the wave index through readfirstlane: the compiler then keeps everything
+  // derived from it in scalar registers and branches on it with scalar tests)
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, l32 = lane & 31, g = lane >> 5;
+  const int qi = q0 + wave * 32 + l32;
+  const int wq_lo = q0 + wave * 32, wq_hi = min(wq_lo + 31, T - 1);
+  const bool wave_live = wq_lo < T;
+
+  // Q^T as the B operand: lane holds query l32, head_dim [16 s + 8 g, +8).
+  bf16x8 qf[C::kKsteps];
+  {
+    const bf16x8* qp = reinterpret_cast<const bf16x8*>(reinterpret_cast<const __bf16*>(d.q) +
+                                                       ((tok0 + min(qi, T - 1)) * H + h) * D);
+#pragma unroll
+    for (int s = 0; s < C::kKsteps; ++s) qf[s] = qp[2 * s + g];
+  }
+
+  // Copies: wave copy i of this wave fills tile rows (wave kDma + i) kRPK +
+  // lane / kCh16; the lane at 16-byte slot p of a row fetches the global chunk
+  // the swizzled layout keeps there (K: chunk c of row r at c ^ (r mod kCh16);
+  // V: 64-byte granule x of row r at x ^ f(r)).  The last tile of a phase
+  // clamps its rows to the last valid one (the extra rows are masked).
+  const uint32_t row_bytes = (uint32_t)(Hkv * D * 2);
+  uint32_t rowb[C::kDma], kchunk[C::kDma], vchunk[C::kDma];
+#pragma unroll
+  for (int i = 0; i < C::kDma; ++i) {
+    const int r = (wave * C::kDma + i) * C::kRPK + lane / C::kCh16;
+    const int p = lane % C::kCh16;
+    const int f = D == 128 ? (r & 3) : ((r >> 1) & 1);
+    rowb[i] = (uint32_t)r * row_bytes;
+    kchunk[i] = (uint32_t)((p ^ (r % C::kCh16)) * 16);
+    vchunk[i] = (uint32_t)((((p >> 2) ^ f) * 4 + (p & 3)) * 16);
+  }
+  const char* kwin = reinterpret_cast<const char*>(reinterpret_cast<const __bf16*>(d.k) + (tok0 * Hkv + hk) * D);
+  const char* vwin = reinterpret_cast<const char*>(reinterpret_cast<const __bf16*>(d.v) + (tok0 * Hkv + hk) * D);
+  const char* kcache = reinterpret_cast<const char*>(
+      reinterpret_cast<const __bf16*>(d.cache_k) + ((int64_t)b * d.cache_cap * Hkv + hk) * D);
+  const char* vcache = reinterpret_cast<const char*>(
+      reinterpret_cast<const __bf16*>(d.cache_v) + ((int64_t)b * d.cache_cap * Hkv + hk) * D);
+  // Copy sources: tile tg starts at (tg < nct ? cache : window - nct tiles) +
+  // tg tiles.  Wave copy i of a tile (K and V) into (kbuf, vbuf); a partial
+  // tile (the last of a phase) clamps its rows to the last valid one.
+  const int64_t tstride = (int64_t)C::kBK * row_bytes;
+  const char* kwin_b = kwin - nct * tstride;
+  const char* vwin_b = vwin - nct * tstride;
+  const int cfull = Cw / C::kBK;               // cache tiles below this are full
+  const int wfull = nct + nwk / C::kBK;        // window tiles in [nct, wfull) are full
+  struct Src {
+    const char* k;
+    const char* v;
+    uint32_t last;  // byte offset of the tile's last valid row (partial tiles)
+    bool full;
+  };
+  auto tile_src = [&](int u) __attribute__((always_inline)) {
+    const int tg = tb + u;
+    const bool in_cache = tg < nct;
+    Src r;
+    r.k = (in_cache ? kcache : kwin_b) + tg * tstride;
+    r.v = (in_cache ? vcache : vwin_b) + tg * tstride;
+    r.full = tg < cfull || (tg >= nct && tg < wfull);
+    r.last = (uint32_t)((in_cache ? Cw : nwk) - 1 - (in_cache ? tg : tg - nct) * C::kBK) * row_bytes;
+    return r;
+  };
+  auto issue = [&](const Src& sr, char* kbuf, char* vbuf, int i, bool clamp) __attribute__((always_inline)) {
+    const uint32_t rb = clamp ? min(rowb[i], sr.last) : rowb[i];
+    const char* ks = sr.k + (rb + kchunk[i]);
+    const char* vs = sr.v + (rb + vchunk[i]);
+    char* kl = kbuf + (wave * C::kDma + i) * 1024;
+    char* vl = vbuf + (wave * C::kDma + i) * 1024;
+    __builtin_amdgcn_global_load_lds(ks, (lds_void*)kl, 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(vs, (lds_void*)vl, 16, 0, 0);
+  };
+
+  // Sub-tile j (32 keys) = half j & 1 of local tile j >> 1, i.e. global
+  // sub-tile J = 2 tb + j: cache rows [32 J, 32 J + 32) while J < 2 nct, then
+  // window rows from 32 (J - 2 nct).  This wave computes sub-tiles j < jlive
+  // (the window rows past its last query are skipped; the cache half-tile
+  // past C_w, if any, is computed fully masked).
+  const int J0 = 2 * tb;
+  const int jlive = wave_live ? min(2 * (tb + ntiles), 2 * nct + (wq_hi >> 5) + 1) - J0 : 0;
+  const int cmask = Cw >> 5;                   // cache sub-tiles from here on reach past C_w
+  const int wmask = 2 * nct + (wq_lo >> 5);    // window sub-tiles from here on reach the diagonal
+  auto need_mask = [&](int J) { return (J >= cmask && J < 2 * nct) || J >= wmask; };
+
+  // LDS operand offsets (lane parts; buffers and sub-tile rows are immediates).
+  // K row 32 half + l32, chunk 2 s + g sits at chunk (2 s + g) ^ (l32 mod kCh16).
+  int kofs[C::kKsteps];
+  {
+    const int kx = g ^ (l32 & (C::kCh16 - 1));
+#pragma unroll
+    for (int s = 0; s < C::kKsteps; ++s) kofs[s] = l32 * C::kRB + (((2 * s) ^ kx) << 4);
+  }
+  // V^T operand: lane = 16 grp + 4 ri + bq reads row 4 (grp / 2) + ri (+ 16 m,
+  // + 8 for the upper half) of the sub-tile, bytes 64 dt + 32 (grp & 1) + 8 bq,
+  // whose 64-byte granule sits at dt ^ f (f = ri, or ri / 2 for D = 64).
+  int vofs[C::kDtiles];
+  {
+    const int grp = lane >> 4, ri = (lane >> 2) & 3, bq = lane & 3;
+    const int f = D == 128 ? ri : (ri >> 1) & 1;
+#pragma unroll
+    for (int dt = 0; dt < C::kDtiles; ++dt)
+      vofs[dt] = (4 * (grp >> 1) + ri) * C::kRB + 32 * (grp & 1) + 8 * bq + ((dt ^ f) << 6);
+  }
+  // Keeps the offsets opaque to loop-invariant code motion, so the compiler
+  // folds buffer and row into the instructions' immediate offsets instead of
+  // holding one address register per (buffer, operand).
+  auto pin_offsets = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int s = 0; s < C::kKsteps; ++s) asm volatile("" : "+v"(kofs[s]));
+#pragma unroll
+    for (int dt = 0; dt < C::kDtiles; ++dt) asm volatile("" : "+v"(vofs[dt]));
+  };
+
+  bf16x8 kop[C::kKsteps];
+  auto read_k = [&](const char* kbuf, int half) __attribute__((always_inline)) {
+#pragma unroll
+    for (int s = 0; s < C::kKsteps; ++s)
+      kop[s] = *reinterpret_cast<const bf16x8*>(kbuf + (kofs[s] + half * 32 * C::kRB));
+  };
+  f32x16 sacc[2];
+  auto qk = [&](f32x16& acc) __attribute__((always_inline)) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[v] = 0.f;
+#pragma unroll
+    for (int s = 0; s < C::kKsteps; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[s], qf[s], acc, 0, 0, 0);
+  };
+
+  f32x16 oacc[C::kDtiles];
+#pragma unroll
+  for (int dt = 0; dt < C::kDtiles; ++dt)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) oacc[dt][v] = 0.f;
+  float m_run = kMinit, l_run = 0.f;
+
+  // One sub-tile iteration (see the header).  half = j & 1 is a constant
+  // after inlining; kc / vc hold tile j >> 1, kn tile (j >> 1) + 1; copies of
+  // tile u + 3 go to (kcp, vcp).
+  auto sub = [&](int j, const int half, const bool fast, const char* vc, const char* kn, char* kcp, char* vcp,
+                 int u, const Src& src) __attribute__((always_inline)) {
+    const bool lj = fast || j < jlive, lj1 = fast || j + 1 < jlive;
+    // A wave keeps at most 15 LDS reads in flight (the counter's range), so
+    // the 16 V^T reads go in two halves around the score MFMAs, and the 8 K
+    // reads follow the softmax's row maximum.  The reads are unconditional (a
+    // dead sub-tile reads a stale but valid buffer), so the compiler's
+    // counter waits stay exact.
+    bf16x8 vop[2 * C::kDtiles];
+    auto read_v = [&](int m) __attribute__((always_inline)) {
+#pragma unroll
+      for (int dt = 0; dt < C::kDtiles; ++dt) {
+        const char* p = vc + (vofs[dt] + (32 * half + 16 * m) * C::kRB);
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)p);
+        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p + 8 * C::kRB));
+        vop[m * C::kDtiles + dt] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
       }
-      __builtin_amdgcn_s_waitcnt(0);  // no copy into LDS outlives the block
-      return;
+    };
+    read_v(0);
+    // S_{j+1}: its K operands were read one sub-tile earlier
+    if (lj1) qk(sacc[half ^ 1]);
+    read_v(1);
+    if (fast || u + 3 < ntiles) {
+#pragma unroll
+      for (int i = 0; i < C::kDma; ++i)
+        if ((i & 1) == half) issue(src, kcp, vcp, i, !fast && !src.full);
     }
-    __syncthreads();
-    for (int t = 0; t < ntiles; t += 3) {
-      compute_tile(tb + t, kbuf0, vbuf0);
-      end_step(false);
-      if (t + 1 >= ntiles) break;
-      compute_tile(tb + t + 1, kbuf1, vbuf1);
-      end_step(false);
-      if (t + 2 >= ntiles) break;
-      compute_tile(tb + t + 2, kbuf2, vbuf2);
-      end_step(false);
+    if (lj) {
+      f32x16& s = sacc[half];
+      const int J = J0 + j;
+      if (!fast && need_mask(J)) {
+        // s[v] = score of query qi with sub-tile key 8 (v/4) + 4 g + v%4
+        const bool c = J < 2 * nct;
+        const int lim_g = (c ? Cw - 32 * J - 1 : qi - 32 * (J - 2 * nct)) - 4 * g;
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          if ((v >> 2) * 8 + (v & 3) > lim_g) s[v] = -INFINITY;
+      }
+      float mx = s[0];
+#pragma unroll
+      for (int v = 1; v < 16; ++v) mx = fmaxf(mx, s[v]);
+      {
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+        mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));  // with lane ^ 32
+      }
+      const float m_new = fmaxf(m_run, mx * sc);
+      if (__any(m_new - m_run > kLazy)) {
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        l_run *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < C::kDtiles; ++dt)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) oacc[dt][v] *= alpha;
+        m_run = m_new;
+      }
     }
+    // K operands of sub-tile j + 2
+    read_k(kn, half);
+    if (lj) {
+      f32x16& s = sacc[half];
+      float psum = 0.f;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(s[v], sc, -m_run));
+        s[v] = p;
+        psum += p;
+      }
+      l_run += psum;
+#pragma unroll
+      for (int m = 0; m < 2; ++m) {
+        bf16x8 pb;
+#pragma unroll
+        for (int v = 0; v < 8; ++v) pb[v] = (__bf16)s[8 * m + v];
+#pragma unroll
+        for (int dt = 0; dt < C::kDtiles; ++dt)
+          oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[m * C::kDtiles + dt], pb, oacc[dt], 0, 0, 0);
+      }
+    }
+  };
+
+  // vmcnt(n): this wave's copies older than its last n have landed
+  auto wait_copies = [&](bool keep_one_step) __attribute__((always_inline)) {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    constexpr int kVm = C::kPerStep;
+    if (keep_one_step)
+      __builtin_amdgcn_s_waitcnt((kVm & 15) | ((kVm >> 4) << 14) | (7 << 4) | (15 << 8));
+    else
+      __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  };
+  // step u: sub-tiles 2u, 2u + 1 from tile u (buffers kc/vc); K of tile u + 1
+  // (kn); copies of tile u + 3 into (kcp, vcp), the buffers tile u - 1 left.
+  // step u: sub-tiles 2u, 2u + 1 from tile u (V in vc); K of tile u + 1
+  // (kn); copies of tile u + 3 into (kcp, vcp), the buffers tile u - 1 left.
+  // A clean step (fast = true) is one of the leading cache steps: every
+  // sub-tile live and unmasked, the copied tile a full cache tile; it runs
+  // without any branch but the softmax's rescaling test.
+  auto step = [&](int u, const char* vc, const char* kn, char* kcp, char* vcp, const bool fast)
+      __attribute__((always_inline)) {
+    pin_offsets();
+    Src src;
+    if (fast) {
+      const int64_t off = (int64_t)(tb + u + 3) * tstride;
+      src.k = kcache + off;
+      src.v = vcache + off;
+      src.last = 0;
+      src.full = true;
+    } else {
+      src = tile_src(u + 3);
+    }
+    sub(2 * u, 0, fast, vc, kn, kcp, vcp, u, src);
+    sub(2 * u + 1, 1, fast, vc, kn, kcp, vcp, u, src);
+    // step u + 1 reads K of tile u + 2: wait for it (tile u + 3 may stay in flight)
+    wait_copies(fast || u + 3 < ntiles);
+  };
+
+  // The scale arrives by a scalar load whose first use is inside the loop;
+  // using it here puts the wait for that load before the loop instead of
+  // (conservatively) at the top of every iteration.
+  asm volatile("" ::"v"(sc));
+  // prologue: tiles 0..2 in flight, wait for 0 and 1
+  {
+    const Src s0 = tile_src(0), s1 = tile_src(1), s2 = tile_src(2);
+#pragma unroll
+    for (int i = 0; i < C::kDma; ++i) {
+      if (ntiles > 0) issue(s0, kb0, vb0, i, !s0.full);
+      if (ntiles > 1) issue(s1, kb1, vb1, i, !s1.full);
+      if (ntiles > 2) issue(s2, kb2, vb2, i, !s2.full);
+    }
+  }
+  wait_copies(ntiles > 2);
+  read_k(kb0, 0);
+  if (0 < jlive) qk(sacc[0]);
+  read_k(kb0, 1);
+  // Let every scalar load land before the loop (lgkmcnt(0) once): a scalar
+  // load still pending there would make the compiler wait for all LDS reads
+  // at every counter wait inside the loop.
+  __builtin_amdgcn_s_waitcnt(0xC07F);
+  // clean steps (a multiple of four, so the general loop starts at stage 0)
+  const int nclean = max(0, min(cfull - tb, ntiles) - 3) & ~3;
+  int u = 0;
+  for (; u < nclean; u += 4) {
+    step(u, vb0, kb1, kb3, vb3, true);
+    step(u + 1, vb1, kb2, kb0, vb0, true);
+    step(u + 2, vb2, kb3, kb1, vb1, true);
+    step(u + 3, vb3, kb0, kb2, vb2, true);
+  }
+  for (; u < ntiles; u += 4) {
+    step(u, vb0, kb1, kb3, vb3, false);
+    if (u + 1 >= ntiles) break;
+    step(u + 1, vb1, kb2, kb0, vb0, false);
+    if (u + 2 >= ntiles) break;
+    step(u + 2, vb2, kb3, kb1, vb1, false);
+    if (u + 3 >= ntiles) break;
+    step(u + 3, vb3, kb0, kb2, vb2, false);
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
@@ -575,10 +884,10 @@ __global__ __launch_bounds__(64 * (W + producer_waves<KL, SQ>()), (W == 1 || pro
     }
     return;
   }
-  if (SQ ? js < nq : qi < T) {
+  if (qi < T) {
     const float inv = 1.f / l_tot;
-    const int64_t orow = SQ ? s0 + js - sq.base : tok0 + qi;
-    __bf16* op = reinterpret_cast<__bf16*>(SQ ? sq.o : d.o) + (orow * H + h) * D;
+    const int64_t orow = tok0 + qi;
+    __bf16* op = reinterpret_cast<__bf16*>(d.o) + (orow * H + h) * D;
 #pragma unroll
     for (int dt = 0; dt < C::kDtiles; ++dt)
 #pragma unroll
@@ -589,8 +898,7 @@ __global__ __launch_bounds__(64 * (W + producer_waves<KL, SQ>()), (W == 1 || pro
         w.y = focus::pack_bf16x2(oacc[dt][4 * v4 + 2] * inv, oacc[dt][4 * v4 + 3] * inv);
         *reinterpret_cast<uint2*>(op + 32 * dt + 8 * v4 + 4 * g) = w;
       }
-    float* lse = SQ ? sq.lse : d.lse;
-    if (g == 0 && lse) lse[orow * H + h] = (m_run + log2f(l_tot)) * kLn2;
+    if (g == 0 && d.lse) d.lse[orow * H + h] = (m_run + log2f(l_tot)) * kLn2;
   }
 }
 
@@ -1091,8 +1399,7 @@ extern "C" focus_status focus_window_attn(const focus_attn_desc* d, focus_stream
   const bool kl = d->mask == FOCUS_MASK_KMER_LOCAL;
   const int waves = kl ? kBf16WavesKL : kBf16Waves;
   const int bq = attn_rows_per_tile(d);
-  // (C(t): one more wave, which copies the tiles)
-  const int threads = d->dtype == FOCUS_BF16 ? 64 * (waves + (kl ? 0 : 1)) : 256;
+  const int threads = d->dtype == FOCUS_BF16 ? 64 * waves : 256;
   const int64_t qt = focus::ceil_div(t.max_window_tokens, bq);
   // Key split when the workspace allows it (else one workgroup per item).
   Split sp = kNoSplit;
@@ -1109,13 +1416,14 @@ extern "C" focus_status focus_window_attn(const focus_attn_desc* d, focus_stream
   if (blocks * threads >= ((int64_t)1 << 32) || qt > INT32_MAX) return FOCUS_E_SHAPE;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const dim3 grid((uint32_t)blocks), block(threads);
-#define FOCUS_ATTN_LAUNCH(KERNEL) hipLaunchKernelGGL(KERNEL, grid, block, 0, s, *d, sc, n_pairs, (int)qt, SumQ{}, sp)
+#define FOCUS_ATTN_LAUNCH(KERNEL) hipLaunchKernelGGL(KERNEL, grid, block, 0, s, *d, sc, n_pairs, (int)qt, SumQ{})
+#define FOCUS_CT_LAUNCH(KERNEL) hipLaunchKernelGGL(KERNEL, grid, block, 0, s, *d, sc, n_pairs, (int)qt, sp)
 #define FOCUS_F32_LAUNCH(KERNEL) hipLaunchKernelGGL(KERNEL, grid, block, 0, s, *d, sc, n_pairs, (int)qt, SumQ{})
   if (d->dtype == FOCUS_BF16) {
     if (d->head_dim == 128) {
-      if (kl) FOCUS_ATTN_LAUNCH((attn_bf16<128, kBf16WavesKL, true, false>)); else FOCUS_ATTN_LAUNCH((attn_bf16<128, kBf16Waves, false, false>));
+      if (kl) FOCUS_ATTN_LAUNCH((attn_bf16<128, kBf16WavesKL, true, false>)); else FOCUS_CT_LAUNCH((attn_ct<128>));
     } else {
-      if (kl) FOCUS_ATTN_LAUNCH((attn_bf16<64, kBf16WavesKL, true, false>)); else FOCUS_ATTN_LAUNCH((attn_bf16<64, kBf16Waves, false, false>));
+      if (kl) FOCUS_ATTN_LAUNCH((attn_bf16<64, kBf16WavesKL, true, false>)); else FOCUS_CT_LAUNCH((attn_ct<64>));
     }
     if (sp.n > 1) {
       const int64_t lanes = sp.nwl * sp.rows * d->n_heads * (d->head_dim / 4);
@@ -1134,6 +1442,7 @@ extern "C" focus_status focus_window_attn(const focus_attn_desc* d, focus_stream
     }
   }
 #undef FOCUS_ATTN_LAUNCH
+#undef FOCUS_CT_LAUNCH
 #undef FOCUS_F32_LAUNCH
   return focus::launch_status();
 }
@@ -1214,7 +1523,7 @@ extern "C" focus_status focus_adapter_attn(const focus_adapter_desc* a, focus_st
   const int64_t blocks = focus::ceil_div(n_pairs, focus::kXcds) * focus::kXcds * qt;
   if (blocks * 64 >= ((int64_t)1 << 32) || qt > INT32_MAX) return FOCUS_E_SHAPE;
   const dim3 grid((uint32_t)blocks), block(64);
-#define FOCUS_SQ_LAUNCH(KERNEL) hipLaunchKernelGGL(KERNEL, grid, block, 0, s, d, sc, n_pairs, (int)qt, sq, kNoSplit)
+#define FOCUS_SQ_LAUNCH(KERNEL) hipLaunchKernelGGL(KERNEL, grid, block, 0, s, d, sc, n_pairs, (int)qt, sq)
   if (a->head_dim == 128) {
     if (kl) FOCUS_SQ_LAUNCH((attn_bf16<128, 1, true, true>)); else FOCUS_SQ_LAUNCH((attn_bf16<128, 1, false, true>));
   } else {
