@@ -35,8 +35,8 @@ HIPCC_FLAGS = [
 
 # Per-source extra flags.  The attention kernels never see a NaN (finite
 # inputs; masked scores are -inf), so their max reductions need no NaN
-# canonicalisation.
-EXTRA_FLAGS = {"window_attn.hip": ["-fno-honor-nans"]}
+# canonicalisation (device code only: the host checks test for NaN).
+EXTRA_FLAGS = {"window_attn.hip": ["-Xarch_device", "-fno-honor-nans"]}
 
 
 def _hipcc() -> str:
