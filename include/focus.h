@@ -348,6 +348,28 @@ size_t focus_decode_workspace(const focus_decode_desc* d);
  * FOCUS_ERR_CAPACITY (the step still attends over what is there). */
 focus_status focus_decode_step(const focus_decode_desc* d, focus_stream_t stream);
 
+/* Bytes of device scratch behind focus_decode_step_noalloc (16 MiB per GPU).
+ * With the automatic split on a 256-CU device and 32 heads x 128, the split
+ * partials (what focus_decode_workspace reports) take under 12 MiB for
+ * batches up to 700 at any cache length; explicit small split_keys values
+ * can need more. */
+#define FOCUS_DECODE_SCRATCH_BYTES (16u << 20)
+
+/* focus_decode_step for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same step, with the split partials kept in a scratch array
+ * of FOCUS_DECODE_SCRATCH_BYTES that the library holds on each GPU it runs on
+ * until the process ends.  d->workspace and d->workspace_bytes are ignored;
+ * every other argument means what it means for focus_decode_step.  The call
+ * allocates nothing (no hipMalloc / hipFree); its first call on a device
+ * looks the array's device address up once.  Every call on one GPU shares
+ * that GPU's array: calls that overlap on one GPU (other streams, other host
+ * threads) race and must be serialised by the caller.
+ * Errors: those of focus_decode_step; E_WORKSPACE when the step's partials
+ * (focus_decode_workspace(d)) exceed FOCUS_DECODE_SCRATCH_BYTES; E_HIP when
+ * the array's address cannot be obtained. */
+focus_status focus_decode_step_noalloc(const focus_decode_desc* d, focus_stream_t stream);
+
 /* ------------------------------------------------------------------------ */
 /* Fidelity metrics                                                          */
 /* ------------------------------------------------------------------------ */

@@ -288,6 +288,25 @@ def focus_decode_step(q, k_new, v_new, kind, cache_k, cache_v, cache_len, win_k,
     return o, lse
 
 
+def focus_decode_step_noalloc(q, k_new, v_new, kind, cache_k, cache_v, cache_len, win_k, win_v, win_len,
+                              o, lse=None, split_keys: int = 0, softmax_scale: float = 0.0, err=None,
+                              stream=None):
+    """focus_decode_step with the partials in the library's per-device scratch
+    array: allocates nothing, so o (and lse, if wanted) must be given."""
+    B, H, D = q.shape
+    Hkv = k_new.shape[1]
+    if (k_new.shape != (B, Hkv, D) or v_new.shape != k_new.shape or kind.numel() < B
+            or cache_k.shape[0] < B or cache_k.shape[2:] != (Hkv, D) or cache_v.shape != cache_k.shape
+            or win_k.shape[0] < B or win_k.shape[2:] != (Hkv, D) or win_v.shape != win_k.shape
+            or cache_len.numel() < B or win_len.numel() < B or o.shape != q.shape
+            or (lse is not None and tuple(lse.shape) != (B, H))):
+        raise ValueError("decode tensor shapes disagree")
+    d = _decode_desc(q, k_new, v_new, kind, cache_k, cache_v, cache_len, win_k, win_v, win_len,
+                     o, lse, None, split_keys, softmax_scale, err)
+    check("focus_decode_step_noalloc", lib().focus_decode_step_noalloc(C.byref(d), _stream(stream, q.device)))
+    return o, lse
+
+
 def focus_fidelity(p, q, input_kind: int = FOCUS_FID_LOGITS, cu_pos=None, out=None, seq_mean=None,
                    err=None, stream=None):
     """Per-position L1 / L2 / Hellinger / JS / KL between the rows of p and q

@@ -128,6 +128,7 @@ SYMBOLS = {
     "focus_window_attn": (i32, [C.POINTER(AttnDesc), p]),
     "focus_decode_workspace": (sz, [C.POINTER(DecodeDesc)]),
     "focus_decode_step": (i32, [C.POINTER(DecodeDesc), p]),
+    "focus_decode_step_noalloc": (i32, [C.POINTER(DecodeDesc), p]),
     "focus_fidelity": (i32, [C.POINTER(FidelityDesc), p]),
     "focus_gemm": (i32, [C.POINTER(GemmDesc), p]),
     "focus_adapter_attn": (i32, [C.POINTER(AdapterDesc), p]),

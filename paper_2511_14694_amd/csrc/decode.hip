@@ -21,6 +21,7 @@
 #include <math.h>
 
 #include <algorithm>
+#include <mutex>
 
 namespace {
 
@@ -281,7 +282,10 @@ extern "C" size_t focus_decode_workspace(const focus_decode_desc* d) {
   return make_plan(d).ws_bytes;
 }
 
-extern "C" focus_status focus_decode_step(const focus_decode_desc* d, focus_stream_t stream) {
+namespace {
+
+// Checks every argument except the workspace; fills the plan.
+focus_status check_step(const focus_decode_desc* d, Plan* p) {
   if (!d) return FOCUS_E_NULL;
   focus_status st = validate(d);
   if (st != FOCUS_OK) return st;
@@ -293,14 +297,19 @@ extern "C" focus_status focus_decode_step(const focus_decode_desc* d, focus_stre
       !focus::aligned16(d->cache_k) || !focus::aligned16(d->cache_v) || !focus::aligned16(d->win_k) ||
       !focus::aligned16(d->win_v) || !focus::aligned16(d->o) || (reinterpret_cast<uintptr_t>(d->lse) & 3u))
     return FOCUS_E_ARG;
-  const Plan p = make_plan(d);
-  if (!d->workspace || d->workspace_bytes < p.ws_bytes) return FOCUS_E_WORKSPACE;
-  if (!focus::aligned16(d->workspace)) return FOCUS_E_ARG;
+  *p = make_plan(d);
+  const int hpb = kThreads / (d->head_dim / kEpt);
+  const int64_t blocks = (int64_t)d->batch * p->n_split * focus::ceil_div(d->n_heads, hpb);
+  if (blocks > INT32_MAX / kThreads) return FOCUS_E_SHAPE;
+  return FOCUS_OK;
+}
+
+// Enqueues the three launches of a step with the partials in ws (at least
+// p.ws_bytes, 16-byte aligned).
+focus_status launch_step(const focus_decode_desc* d, const Plan& p, void* ws, hipStream_t s) {
+  focus_status st;
   const int hpb = kThreads / (d->head_dim / kEpt);
   const int64_t blocks = (int64_t)d->batch * p.n_split * focus::ceil_div(d->n_heads, hpb);
-  if (blocks > INT32_MAX / kThreads) return FOCUS_E_SHAPE;
-
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const int64_t eb = focus::elt_bytes(d->dtype);
   const int64_t row_u4 = (int64_t)d->n_kv_heads * d->head_dim * eb / 16;
   hipLaunchKernelGGL(decode_append, dim3(d->batch), dim3(256), 0, s, *d, row_u4);
@@ -308,9 +317,9 @@ extern "C" focus_status focus_decode_step(const focus_decode_desc* d, focus_stre
 
   const float scale = d->softmax_scale > 0.f ? d->softmax_scale : 1.0f / sqrtf((float)d->head_dim);
   const float sc = scale * kLog2e;
-  float* ws_o = reinterpret_cast<float*>(d->workspace);
-  float* ws_ml = reinterpret_cast<float*>(reinterpret_cast<char*>(d->workspace) + p.ml_offset);
-  int32_t* ws_n = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(d->workspace) + p.n_offset);
+  float* ws_o = reinterpret_cast<float*>(ws);
+  float* ws_ml = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + p.ml_offset);
+  int32_t* ws_n = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(ws) + p.n_offset);
   const dim3 block(kThreads);
 #define FOCUS_DECODE_LAUNCH(T, D)                                                                  \
   hipLaunchKernelGGL((decode_partial<T, D>), dim3((uint32_t)blocks), block, 0, s, *d, sc, p.split, \
@@ -325,4 +334,56 @@ extern "C" focus_status focus_decode_step(const focus_decode_desc* d, focus_stre
   }
 #undef FOCUS_DECODE_LAUNCH
   return focus::launch_status();
+}
+
+}  // namespace
+
+extern "C" focus_status focus_decode_step(const focus_decode_desc* d, focus_stream_t stream) {
+  Plan p;
+  const focus_status st = check_step(d, &p);
+  if (st != FOCUS_OK || d->batch == 0) return st;
+  if (!d->workspace || d->workspace_bytes < p.ws_bytes) return FOCUS_E_WORKSPACE;
+  if (!focus::aligned16(d->workspace)) return FOCUS_E_ARG;
+  return launch_step(d, p, d->workspace, reinterpret_cast<hipStream_t>(stream));
+}
+
+// ------------------------------------------------ allocation-free variant
+
+// The partials of focus_decode_step_noalloc live in this array: one copy per
+// device, held until the process ends.  Host code never passes the array's
+// name to a kernel (on the host it is only a stand-in for the symbol): the
+// device address comes from hipGetSymbolAddress, looked up once per device
+// with that device current.
+static __device__ __align__(256) char scratch[FOCUS_DECODE_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+// Device address of this device's scratch array (looked up on first use).
+focus_status scratch_address(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return FOCUS_E_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return FOCUS_E_HIP;
+    g_scratch[dev] = ptr;
+  }
+  *out = g_scratch[dev];
+  return FOCUS_OK;
+}
+
+}  // namespace
+
+extern "C" focus_status focus_decode_step_noalloc(const focus_decode_desc* d, focus_stream_t stream) {
+  Plan p;
+  focus_status st = check_step(d, &p);
+  if (st != FOCUS_OK || d->batch == 0) return st;
+  if (p.ws_bytes > (size_t)FOCUS_DECODE_SCRATCH_BYTES) return FOCUS_E_WORKSPACE;
+  void* ws = nullptr;
+  if ((st = scratch_address(&ws)) != FOCUS_OK) return st;
+  return launch_step(d, p, ws, reinterpret_cast<hipStream_t>(stream));
 }
