@@ -35,16 +35,25 @@ from .layout import BASE, SUMMARY
 class DecodeSequence:
     """Decode state of one sequence (see module docstring)."""
 
-    def __init__(self, window_nt: int, kmer: int, cache_k, cache_v, win_k, win_v,
+    def __init__(self, window_nt: int, kmer, cache_k, cache_v, win_k, win_v,
                  bases_in_window: int, bases_in_kmer: int):
+        """kmer: one cadence for every window, or the cadences of the current
+        window and of the windows after it (the last entry repeats), as the
+        layout allows one k_w per window."""
         self.W = int(window_nt)
-        self.k = int(kmer)
+        self.cadences = [int(kmer)] if np.ndim(kmer) == 0 else [int(x) for x in kmer]
+        self.win_index = 0      # windows closed since the start
         self.cache_k = [np.asarray(r) for r in cache_k]
         self.cache_v = [np.asarray(r) for r in cache_v]
         self.win_k = [np.asarray(r) for r in win_k]
         self.win_v = [np.asarray(r) for r in win_v]
         self.bases_in_window = int(bases_in_window)
         self.bases_in_kmer = int(bases_in_kmer)
+
+    @property
+    def k(self) -> int:
+        """Cadence of the current window."""
+        return self.cadences[min(self.win_index, len(self.cadences) - 1)]
 
     @staticmethod
     def replay_counters(window_nt: int, kmer: int, n_tokens: int):
@@ -89,6 +98,7 @@ class DecodeSequence:
             self.win_k, self.win_v = [], []
             self.bases_in_window = 0
             self.bases_in_kmer = 0
+            self.win_index += 1
         return o, lse, kind, window_end
 
     def attend(self, q, scale=None):

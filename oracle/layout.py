@@ -26,6 +26,8 @@ Indexing conventions (shared with the C interface, 0-based):
   tok_pos              index of the token inside its own sequence's stream
   tok_kmer             cache row (inside its sequence) of the summary that
                        closes the token's k-mer; -1 when the window has k_w = 0
+  tok_next_base        global base index of pi(t), the first real base after
+                       token t in its sequence (Appendix A.1, eq. loss), or -1
 """
 
 from __future__ import annotations
@@ -128,6 +130,17 @@ def build_layout(seq_nt, window_nt: int, kmer, bases=None, summary_token_id: int
         cu_tokens.append(g_token)
         cu_summaries.append(g_summary)
 
+    # Target map of the training objective (Appendix A.1, eq. loss): for every
+    # position t, pi(t) is the first real-base position after t; recorded as
+    # that base's global index, -1 when t is past its sequence's last base.
+    next_base = [-1] * g_token
+    for b in range(len(seq_nt)):
+        nxt = -1
+        for t in range(cu_tokens[b + 1] - 1, cu_tokens[b] - 1, -1):
+            next_base[t] = nxt
+            if tok["kind"][t] == BASE:
+                nxt = tok["base"][t]
+
     i32, i64 = np.int32, np.int64
     out = {
         "n_windows": g_window,
@@ -149,6 +162,7 @@ def build_layout(seq_nt, window_nt: int, kmer, bases=None, summary_token_id: int
         "tok_base": np.asarray(tok["base"], i64),
         "tok_kmer": np.asarray(tok["kmer"], i32),
         "tok_win": np.asarray(tok["win"], i32),
+        "tok_next_base": np.asarray(next_base, i64),
         "sum_tok": np.asarray(sum_tok, i64),
         "window_kmer": np.asarray(kmer_of, i32),
     }

@@ -80,3 +80,29 @@ def test_cache_growth_and_window_reset():
     assert "".join("S" if x == SUMMARY else "b" for x in kinds) == one * 3
     assert [i for i, e in enumerate(ends) if e] == [12, 25, 38]
     assert cache[-1] == 9 and win[12] == 0 and win[11] == 10
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_per_window_cadence_equals_prefill(seed):
+    """Windows with their own cadence k_w (the layout allows one per window):
+    decoding from empty through several windows, the cadence switching at each
+    window end, gives the prefill rows of the same per-window layout."""
+    rng = np.random.default_rng(50 + seed)
+    W = int(rng.integers(5, 12))
+    L = 4 * W
+    km = rng.choice([1, 2, 3, 5, 50], 4).astype(np.int32)
+    lay = build_layout([L], W, km)
+    NT = lay["n_tokens"]
+    q = rng.standard_normal((NT, 2, 4))
+    kk = rng.standard_normal((NT, 1, 4))
+    v = rng.standard_normal((NT, 1, 4))
+    o_ref, l_ref = A.prefill_sequential(lay, q, kk, v)
+    st = DecodeSequence(W, km, [], [], [], [], 0, 0)
+    for t in range(NT):
+        o, lse, kind, end = st.step(q[t], kk[t], v[t])
+        w = lay["tok_win"][t]
+        assert kind == lay["tok_kind"][t]
+        assert end == (t == lay["win_tok_off"][w] + lay["win_ntok"][w] - 1)
+        np.testing.assert_allclose(o, o_ref[t], rtol=1e-12, atol=1e-13)
+        np.testing.assert_allclose(lse, l_ref[t], rtol=1e-12, atol=1e-13)
+    assert st.cache_len == lay["n_summaries"] and st.win_index == 4

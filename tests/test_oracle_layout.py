@@ -192,3 +192,52 @@ def test_ragged_workload_counts():
     per_seq = np.diff(lay["cu_summaries"])
     assert len(set(per_seq.tolist())) > 1
     assert per_seq.sum() == lay["n_summaries"] == int((1000 // kmer).sum())
+
+
+# ---- target map pi(t) (Appendix A.1, eq. loss) ----
+
+def _next_base_cases():
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "next_base_worked_examples.txt")
+    cases = []
+    for line in open(path):
+        if line.startswith("#") or not line.strip():
+            continue
+        head, stream, pi = (x.strip() for x in line.split("|"))
+        lens, W, k = head.split()
+        cases.append(([int(x) for x in lens.split(",")], int(W), int(k), stream, [int(x) for x in pi.split()]))
+    return cases
+
+
+@pytest.mark.parametrize("seq,W,k,stream,pi", _next_base_cases())
+def test_next_base_worked_examples(seq, W, k, stream, pi):
+    lay = build_layout(seq, W, k)
+    toks = stream.replace("/", " ").replace(";", " ").split()
+    assert len(toks) == lay["n_tokens"]
+    for t, s in enumerate(toks):
+        assert (lay["tok_kind"][t] == SUMMARY) == (s == "S")
+        if s != "S":
+            assert lay["tok_base"][t] == int(s[1:])
+    assert lay["tok_next_base"].tolist() == pi
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_next_base_brute_force(seed):
+    """pi(t) = min{u > t : u a real base} by literal search over the stream,
+    on random batches with per-window cadences (k = 0 windows included)."""
+    rng = np.random.default_rng(100 + seed)
+    seq = [int(x) for x in rng.integers(0, 40, 3)]
+    W = int(rng.integers(1, 12))
+    nw = sum(-(-L // W) for L in seq)
+    km = rng.integers(0, 6, nw).astype(np.int32)
+    lay = build_layout(seq, W, km)
+    kind, base, cu = lay["tok_kind"], lay["tok_base"], lay["cu_tokens"]
+    for b in range(len(seq)):
+        for t in range(cu[b], cu[b + 1]):
+            later = [u for u in range(t + 1, cu[b + 1]) if kind[u] == BASE]
+            want = base[min(later)] if later else -1
+            assert lay["tok_next_base"][t] == want
+    # a real base's target is the next base of its sequence
+    for t in np.nonzero(kind == BASE)[0]:
+        b = int(np.searchsorted(cu, t, side="right") - 1)
+        last = sum(seq[:b + 1]) - 1
+        assert lay["tok_next_base"][t] == (base[t] + 1 if base[t] < last else -1)

@@ -49,6 +49,10 @@ def _layout_pins():
         TL.test_appendix_a_closed_forms(seed)
         TL.test_kmer_membership_and_positions(seed)
         TL.test_literal_string_insertion(seed)
+    for case in TL._next_base_cases():
+        TL.test_next_base_worked_examples(*case)
+    for seed in range(6):
+        TL.test_next_base_brute_force(seed)
 
 
 def _attention_pins():
@@ -116,6 +120,8 @@ def _decode_pins():
     TD.test_decode_from_empty_equals_prefill(25, 7, 7)
     TD.test_decode_mid_window_start_equals_prefill(11)
     TD.test_cache_growth_and_window_reset()
+    for seed in range(4):
+        TD.test_per_window_cadence_equals_prefill(seed)
 
 
 ATTENTION_MUTATIONS = [
@@ -147,6 +153,10 @@ LAYOUT_MUTATIONS = [
     ("window one base short", "stop = min(start + W, L)", "stop = min(start + W - 1, L)"),
     ("kmer row of next summary", "emit(BASE, g_base0 + i, cache_rows + j if k > 0 else -1)",
      "emit(BASE, g_base0 + i, cache_rows + j + 1 if k > 0 else -1)"),
+    ("target is the token itself", "            next_base[t] = nxt\n            if tok[\"kind\"][t] == BASE:",
+     "            if tok[\"kind\"][t] == BASE:\n                next_base[t] = tok[\"base\"][t]\n            if tok[\"kind\"][t] == BASE:"),
+    ("target carried across sequences", "    for b in range(len(seq_nt)):\n        nxt = -1\n",
+     "    nxt = -1\n    for b in range(len(seq_nt)):\n"),
 ]
 
 DECODE_MUTATIONS = [
@@ -154,6 +164,7 @@ DECODE_MUTATIONS = [
     ("window never reset", "self.win_k, self.win_v = [], []", "pass"),
     ("summary into window buffer", "self.cache_k.append(np.asarray(k_new))",
      "self.win_k.append(np.asarray(k_new))"),
+    ("cadence never switches", "            self.win_index += 1\n", "            pass\n"),
 ]
 
 
