@@ -49,7 +49,7 @@
 extern "C" {
 #endif
 
-#define FOCUS_ABI_VERSION 2
+#define FOCUS_ABI_VERSION 3
 
 typedef int32_t focus_status;
 enum {
@@ -91,7 +91,8 @@ int32_t focus_abi_version(void);
 const char* focus_status_str(focus_status s);
 /* sizeof of the descriptor structs below, in declaration order
  * (0 totals, 1 layout, 2 compact, 3 attn, 4 decode, 5 fidelity, 6 gemm,
- * 7 adapter, 8 adapter layer, 9 qkv projection); -1 otherwise.
+ * 7 adapter, 8 adapter layer, 9 qkv projection, 10 decode schedule); -1
+ * otherwise.
  * Lets a binding check its mirror of the structs. */
 int64_t focus_struct_size(int32_t which);
 
@@ -135,7 +136,10 @@ focus_status focus_layout_plan(int32_t batch, const int64_t* seq_nt, int32_t win
  * tok_kind[t] (FOCUS_TOK_*), tok_pos[t] = position in its sequence's augmented
  * stream, tok_win[t] = window, tok_base[t] = global base index or -1 for a
  * summary, tok_kmer[t] = cache row of the summary closing its k-mer (-1 when
- * k_w = 0), token_ids[t] = bases[tok_base[t]] or summary_token_id.
+ * k_w = 0), token_ids[t] = bases[tok_base[t]] or summary_token_id, and, if
+ * asked for, tok_next_base[t] = the global base index of pi(t), the first real
+ * base after t in its sequence (the training target of every position,
+ * Appendix A.1 eq. loss), or -1 past the sequence's last base.
  * Per summary s: sum_tok[s] = its global token index.
  * cu_*[b] = first global window / token / summary of sequence b; cu_*[batch] =
  * the total. */
@@ -166,6 +170,7 @@ typedef struct {
   int64_t* tok_base;
   int64_t* sum_tok;             /* [n_summaries]                             */
   int32_t* token_ids;           /* [n_tokens], written only if bases != NULL */
+  int64_t* tok_next_base;       /* [n_tokens] or NULL: pi(t), see above      */
   int32_t* err;                 /* optional error word                       */
 } focus_layout_desc;
 
@@ -304,8 +309,9 @@ focus_status focus_window_attn(const focus_attn_desc* d, focus_stream_t stream);
  *   2. o[b, h] = softmax(scale * q[b, h] . [cache[0:cache_len] ;
  *      win[0:win_len]]^T) . values, every row visible; lse likewise;
  *   3. if kind[b] & FOCUS_STEP_WINDOW_END, set win_len[b] = 0 afterwards.
- * The caller derives kind from the layout (a summary every k bases, the last
- * summary of a window ends it).  Keys are split into chunks of split_keys rows
+ * focus_decode_next_kind derives kind on the device from each sequence's
+ * position in the layout (a summary every k bases, the last summary of a
+ * window ends it).  Keys are split into chunks of split_keys rows
  * processed in parallel and merged by log-sum-exp; results do not depend on
  * the split beyond float32 rounding, and are deterministic for a fixed split.
  * All state lives in device memory, so steps can be enqueued back to back
@@ -347,6 +353,49 @@ size_t focus_decode_workspace(const focus_decode_desc* d);
  * An append into a full cache or window buffer is skipped with
  * FOCUS_ERR_CAPACITY (the step still attends over what is there). */
 focus_status focus_decode_step(const focus_decode_desc* d, focus_stream_t stream);
+
+/* Decode schedule: where each sequence of a decode batch stands in the
+ * summary layout, followed token by token (the insertion rule of Section 3.2
+ * and Appendix A: a summary after every k_w bases of window w, a trailing
+ * partial k-mer closed by one at the window's end; Appendix A.2 streaming).
+ * The next token of sequence b is a summary when its window's cadence k > 0
+ * and either the open k-mer holds k bases or the window holds W bases with a
+ * k-mer open; it ends the window when it is that window's last summary (or,
+ * for k = 0, its W-th base).  All arrays [device][batch] unless noted. */
+typedef struct {
+  int32_t batch;
+  int32_t window_nt;            /* W, bases per window, >= 1                 */
+  int32_t kmer_uniform;         /* cadence of every window when kmer == NULL */
+  int32_t kmer_stride;          /* cadences per sequence in kmer (>= 1)      */
+  const int32_t* kmer;          /* [batch][kmer_stride] or NULL: cadence of
+                                   window j of sequence b at
+                                   kmer[b * kmer_stride + min(j, stride - 1)] */
+  int32_t* win_index;           /* in/out: the sequence's current window j   */
+  int32_t* bases_in_window;     /* in/out: bases of window j so far          */
+  int32_t* bases_in_kmer;       /* in/out: bases of its open k-mer           */
+  uint8_t* kind;                /* out, focus_decode_next_kind: FOCUS_STEP_*
+                                   bits of the next token (the kind argument
+                                   of focus_decode_step)                     */
+  const int32_t* tokens;        /* in, focus_decode_sched_start: tokens of
+                                   window j already in the cache / window    */
+  int32_t* summaries;           /* out, focus_decode_sched_start (or NULL):
+                                   how many of those tokens are summaries    */
+  int32_t* err;                 /* optional error word                       */
+} focus_decode_sched;
+
+/* Set bases_in_window / bases_in_kmer of every sequence by walking tokens[b]
+ * tokens from the start of its window win_index[b] with the rule above (a
+ * walk that closes the window moves on to the next one); summaries[b] gets
+ * the number of summary tokens walked.  Use it to start decoding part-way
+ * into a window.  A negative cadence raises FOCUS_ERR_BOUNDS and counts as 0.
+ * Errors: E_NULL, E_ARG, E_HIP. */
+focus_status focus_decode_sched_start(const focus_decode_sched* s, focus_stream_t stream);
+
+/* Derive the kind of every sequence's next token into s->kind and advance
+ * the counters past it (a window end moves to the next window).  Enqueue it
+ * before each focus_decode_step that takes s->kind.  Errors: E_NULL, E_ARG,
+ * E_HIP. */
+focus_status focus_decode_next_kind(const focus_decode_sched* s, focus_stream_t stream);
 
 /* Bytes of device scratch behind focus_decode_step_noalloc (16 MiB per GPU).
  * With the automatic split on a 256-CU device and 32 heads x 128, the split

@@ -23,7 +23,7 @@ from typing import Dict, Optional
 import numpy as np
 import torch
 
-from ._abi import (AdapterDesc, AdapterLayerDesc, AttnDesc, CompactDesc, DecodeDesc, FidelityDesc, FocusError, GemmDesc, LayoutDesc, LayoutTotals, QkvDesc,
+from ._abi import (AdapterDesc, AdapterLayerDesc, AttnDesc, CompactDesc, DecodeDesc, DecodeSched, FidelityDesc, FocusError, GemmDesc, LayoutDesc, LayoutTotals, QkvDesc,
                    FOCUS_BF16, FOCUS_F32, FOCUS_MASK_CT, FOCUS_MASK_KMER_LOCAL,
                    FOCUS_TOK_BASE, FOCUS_TOK_SUMMARY, FOCUS_STEP_SUMMARY, FOCUS_STEP_WINDOW_END,
                    FOCUS_ERR_CAPACITY, FOCUS_ERR_BOUNDS, FOCUS_ERR_PLAN,
@@ -31,6 +31,7 @@ from ._abi import (AdapterDesc, AdapterLayerDesc, AttnDesc, CompactDesc, DecodeD
 
 __all__ = ["focus_layout_plan", "focus_layout", "focus_compact_kv", "focus_window_attn",
            "focus_window_attn_workspace", "focus_decode_step", "focus_decode_workspace",
+           "focus_decode_step_noalloc", "DecodeSchedule",
            "focus_fidelity", "focus_gemm", "focus_adapter_attn", "focus_adapter_layer",
            "focus_adapter_layer_workspace", "focus_qkv_project", "focus_abi_version", "Layout", "LayoutTotals", "FocusError",
            "FOCUS_FID_LOGITS", "FOCUS_FID_PROBS", "FOCUS_FID_N",
@@ -48,7 +49,8 @@ _FIELD_DTYPE = {"cu_windows": torch.int64, "cu_tokens": torch.int64, "cu_summari
                 "win_ntok": torch.int32, "win_cache_off": torch.int32, "win_tok_off": torch.int64,
                 "win_sum_off": torch.int64, "win_base_off": torch.int64, "tok_pos": torch.int32,
                 "tok_kmer": torch.int32, "tok_win": torch.int32, "tok_kind": torch.uint8,
-                "tok_base": torch.int64, "sum_tok": torch.int64, "token_ids": torch.int32}
+                "tok_base": torch.int64, "sum_tok": torch.int64, "token_ids": torch.int32,
+                "tok_next_base": torch.int64}
 
 
 def focus_abi_version() -> int:
@@ -74,6 +76,17 @@ def _stream(stream, device) -> int:
     if stream is None:
         stream = torch.cuda.current_stream(device)
     return stream.cuda_stream
+
+
+def _scratch(nbytes: int, device, stream):
+    """Scratch for the duration of one call: allocated on the stream the call's
+    kernels run on, so the caching allocator hands the block to other work only
+    behind them once it is freed (on the caller's current stream when stream is
+    None)."""
+    if stream is None:
+        return torch.empty(nbytes, dtype=torch.uint8, device=device)
+    with torch.cuda.stream(stream):
+        return torch.empty(nbytes, dtype=torch.uint8, device=device)
 
 
 def _dtype(t) -> int:
@@ -113,10 +126,11 @@ class Layout:
 
 def focus_layout(totals: LayoutTotals, seq_nt, window_nt: int, kmer=None, kmer_uniform: int = 0,
                  bases=None, summary_token_id: int = 0, err=None, device="cuda", stream=None,
-                 out: Optional[Layout] = None) -> Layout:
+                 out: Optional[Layout] = None, next_base: bool = False) -> Layout:
     """Fill the layout arrays on the device.  seq_nt / kmer / bases may be host
     arrays (copied to the device) or device tensors.  `out`: a Layout of the
-    same totals whose arrays are written again instead of allocating new ones."""
+    same totals whose arrays are written again instead of allocating new ones.
+    next_base: also fill tok_next_base (the target map pi(t))."""
     dev = torch.device(device)
     seq = torch.as_tensor(np.asarray(seq_nt, dtype=np.int64) if not torch.is_tensor(seq_nt) else seq_nt,
                           dtype=torch.int64).to(dev).contiguous()
@@ -135,6 +149,8 @@ def focus_layout(totals: LayoutTotals, seq_nt, window_nt: int, kmer=None, kmer_u
     sizes.update({f: totals.n_tokens for f in TOKEN_FIELDS})
     if bs is not None:
         sizes["token_ids"] = totals.n_tokens
+    if next_base:
+        sizes["tok_next_base"] = totals.n_tokens
     if out is not None:
         arrays = out.arrays
         if any(f not in arrays or arrays[f].numel() != max(int(n), 0) for f, n in sizes.items()):
@@ -206,8 +222,9 @@ def _attn_desc(lay, q, k, v, cache_k, cache_v, o, lse, win_ids, qkv_tok_base, so
     return d
 
 
-def focus_window_attn_workspace(lay: Layout, q, k, v, cache_k=None, cache_v=None, win_ids=None) -> int:
-    d = _attn_desc(lay, q, k, v, cache_k, cache_v, None, None, win_ids, 0, 0.0, FOCUS_MASK_CT, None, None)
+def focus_window_attn_workspace(lay: Layout, q, k, v, cache_k=None, cache_v=None, win_ids=None,
+                                mask: int = FOCUS_MASK_CT) -> int:
+    d = _attn_desc(lay, q, k, v, cache_k, cache_v, None, None, win_ids, 0, 0.0, mask, None, None)
     return lib().focus_window_attn_workspace(C.byref(d))
 
 
@@ -227,8 +244,8 @@ def focus_window_attn(lay: Layout, q, k, v, cache_k=None, cache_v=None, o=None, 
         raise ValueError("o must match q; lse must be [rows, heads]")
     if workspace is None:
         # key-split scratch for launches that would leave compute units idle
-        n = focus_window_attn_workspace(lay, q, k, v, cache_k, cache_v, win_ids)
-        workspace = torch.empty(n, dtype=torch.uint8, device=q.device) if n > 0 else None
+        n = focus_window_attn_workspace(lay, q, k, v, cache_k, cache_v, win_ids, mask)
+        workspace = _scratch(n, q.device, stream) if n > 0 else None
     d = _attn_desc(lay, q, k, v, cache_k, cache_v, o, lse, win_ids, qkv_tok_base, softmax_scale,
                    mask, workspace, err)
     check("focus_window_attn", lib().focus_window_attn(C.byref(d), _stream(stream, q.device)))
@@ -281,11 +298,64 @@ def focus_decode_step(q, k_new, v_new, kind, cache_k, cache_v, cache_len, win_k,
         raise ValueError("decode tensor shapes disagree")
     if workspace is None:
         n = focus_decode_workspace(q, k_new, cache_k, win_k, split_keys)
-        workspace = torch.empty(max(n, 16), dtype=torch.uint8, device=q.device)
+        workspace = _scratch(max(n, 16), q.device, stream)
     d = _decode_desc(q, k_new, v_new, kind, cache_k, cache_v, cache_len, win_k, win_v, win_len,
                      o, lse, workspace, split_keys, softmax_scale, err)
     check("focus_decode_step", lib().focus_decode_step(C.byref(d), _stream(stream, q.device)))
     return o, lse
+
+
+class DecodeSchedule:
+    """Device-side decode schedule of a batch (focus_decode_sched): each
+    sequence's current window, bases in it and bases in its open k-mer.
+
+    kmer: None (kmer_uniform for every window) or [batch, n] cadences of the
+    windows j = 0, 1, ... of each sequence (the last one repeats); win_index:
+    each sequence's current window (default 0)."""
+
+    def __init__(self, batch: int, window_nt: int, kmer=None, kmer_uniform: int = 0, win_index=None,
+                 device="cuda", err=None):
+        dev = torch.device(device)
+        self.batch, self.window_nt, self.kmer_uniform = int(batch), int(window_nt), int(kmer_uniform)
+        self.kmer = None
+        if kmer is not None:
+            km = torch.as_tensor(np.asarray(kmer, np.int32) if not torch.is_tensor(kmer) else kmer,
+                                 dtype=torch.int32).to(dev).contiguous()
+            if km.dim() != 2 or km.shape[0] != batch or km.shape[1] < 1:
+                raise ValueError("kmer must be [batch, windows]")
+            self.kmer = km
+        z = lambda dt: torch.zeros(batch, dtype=dt, device=dev)   # noqa: E731
+        self.win_index = z(torch.int32) if win_index is None else \
+            torch.as_tensor(win_index, dtype=torch.int32).to(dev).contiguous()
+        self.bases_in_window, self.bases_in_kmer = z(torch.int32), z(torch.int32)
+        self.kind = z(torch.uint8)
+        self.summaries = z(torch.int32)
+        self.err = err
+
+    def _desc(self, tokens=None):
+        d = DecodeSched()
+        d.batch, d.window_nt, d.kmer_uniform = self.batch, self.window_nt, self.kmer_uniform
+        d.kmer_stride = 0 if self.kmer is None else self.kmer.shape[1]
+        d.kmer = _ptr(self.kmer)
+        d.win_index, d.bases_in_window = _ptr(self.win_index), _ptr(self.bases_in_window)
+        d.bases_in_kmer, d.kind = _ptr(self.bases_in_kmer), _ptr(self.kind)
+        d.tokens, d.summaries, d.err = _ptr(tokens), _ptr(self.summaries), _ptr(self.err)
+        return d
+
+    def start(self, tokens, stream=None):
+        """Walk tokens[b] tokens into each sequence's current window; returns
+        the device tensor of how many of them are summaries."""
+        t = torch.as_tensor(tokens, dtype=torch.int32).to(self.kind.device).contiguous()
+        d = self._desc(t)
+        check("focus_decode_sched_start", lib().focus_decode_sched_start(C.byref(d),
+                                                                       _stream(stream, self.kind.device)))
+        return self.summaries
+
+    def next_kind(self, stream=None):
+        """Derive the next token's kinds into self.kind (returned) and advance."""
+        d = self._desc()
+        check("focus_decode_next_kind", lib().focus_decode_next_kind(C.byref(d), _stream(stream, self.kind.device)))
+        return self.kind
 
 
 def focus_decode_step_noalloc(q, k_new, v_new, kind, cache_k, cache_v, cache_len, win_k, win_v, win_len,
@@ -423,8 +493,9 @@ def _adapter_layer_desc(lay: Layout, hidden, w_q, w_k, w_v, w_o, n_heads, n_kv_h
     return d
 
 
-def focus_adapter_layer_workspace(lay: Layout, hidden, w_q, w_k, w_v, w_o, n_heads: int, n_kv_heads: int) -> int:
-    d = _adapter_layer_desc(lay, hidden, w_q, w_k, w_v, w_o, n_heads, n_kv_heads, FOCUS_MASK_CT, 0.0,
+def focus_adapter_layer_workspace(lay: Layout, hidden, w_q, w_k, w_v, w_o, n_heads: int, n_kv_heads: int,
+                                  mask: int = FOCUS_MASK_CT) -> int:
+    d = _adapter_layer_desc(lay, hidden, w_q, w_k, w_v, w_o, n_heads, n_kv_heads, mask, 0.0,
                             None, None, None)
     return lib().focus_adapter_layer_workspace(C.byref(d))
 
@@ -437,8 +508,8 @@ def focus_adapter_layer(lay: Layout, hidden, w_q, w_k, w_v, w_o, n_heads: int, n
     if out is None:
         out = torch.empty(lay.totals.n_summaries, hidden.shape[1], dtype=hidden.dtype, device=hidden.device)
     if workspace is None:
-        n = focus_adapter_layer_workspace(lay, hidden, w_q, w_k, w_v, w_o, n_heads, n_kv_heads)
-        workspace = torch.empty(max(n, 256), dtype=torch.uint8, device=hidden.device)
+        n = focus_adapter_layer_workspace(lay, hidden, w_q, w_k, w_v, w_o, n_heads, n_kv_heads, mask)
+        workspace = _scratch(max(n, 256), hidden.device, stream)
     d = _adapter_layer_desc(lay, hidden, w_q, w_k, w_v, w_o, n_heads, n_kv_heads, mask, softmax_scale,
                             out, workspace, err)
     check("focus_adapter_layer", lib().focus_adapter_layer(C.byref(d), _stream(stream, hidden.device)))

@@ -40,7 +40,7 @@ class LayoutDesc(C.Structure):
                 ("win_seq", p), ("win_nt", p), ("win_nsum", p), ("win_ntok", p),
                 ("win_cache_off", p), ("win_tok_off", p), ("win_sum_off", p), ("win_base_off", p),
                 ("tok_pos", p), ("tok_kmer", p), ("tok_win", p), ("tok_kind", p), ("tok_base", p),
-                ("sum_tok", p), ("token_ids", p), ("err", p)]
+                ("sum_tok", p), ("token_ids", p), ("tok_next_base", p), ("err", p)]
 
 
 class CompactDesc(C.Structure):
@@ -69,6 +69,12 @@ class DecodeDesc(C.Structure):
                 ("cache_k", p), ("cache_v", p), ("cache_cap", i64), ("cache_len", p),
                 ("win_k", p), ("win_v", p), ("win_cap", i64), ("win_len", p),
                 ("o", p), ("lse", p), ("workspace", p), ("workspace_bytes", sz), ("err", p)]
+
+
+class DecodeSched(C.Structure):
+    _fields_ = [("batch", i32), ("window_nt", i32), ("kmer_uniform", i32), ("kmer_stride", i32),
+                ("kmer", p), ("win_index", p), ("bases_in_window", p), ("bases_in_kmer", p),
+                ("kind", p), ("tokens", p), ("summaries", p), ("err", p)]
 
 
 class FidelityDesc(C.Structure):
@@ -114,7 +120,7 @@ class QkvDesc(C.Structure):
 
 
 STRUCTS = [LayoutTotals, LayoutDesc, CompactDesc, AttnDesc, DecodeDesc, FidelityDesc, GemmDesc, AdapterDesc,
-           AdapterLayerDesc, QkvDesc]
+           AdapterLayerDesc, QkvDesc, DecodeSched]
 
 # name -> (restype, argtypes): every symbol include/focus.h declares
 SYMBOLS = {
@@ -129,6 +135,8 @@ SYMBOLS = {
     "focus_decode_workspace": (sz, [C.POINTER(DecodeDesc)]),
     "focus_decode_step": (i32, [C.POINTER(DecodeDesc), p]),
     "focus_decode_step_noalloc": (i32, [C.POINTER(DecodeDesc), p]),
+    "focus_decode_sched_start": (i32, [C.POINTER(DecodeSched), p]),
+    "focus_decode_next_kind": (i32, [C.POINTER(DecodeSched), p]),
     "focus_fidelity": (i32, [C.POINTER(FidelityDesc), p]),
     "focus_gemm": (i32, [C.POINTER(GemmDesc), p]),
     "focus_adapter_attn": (i32, [C.POINTER(AdapterDesc), p]),

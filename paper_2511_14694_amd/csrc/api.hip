@@ -31,6 +31,7 @@ extern "C" int64_t focus_struct_size(int32_t which) {
     case 7: return sizeof(focus_adapter_desc);
     case 8: return sizeof(focus_adapter_layer_desc);
     case 9: return sizeof(focus_qkv_desc);
+    case 10: return sizeof(focus_decode_sched);
     default: return -1;
   }
 }

@@ -347,6 +347,91 @@ extern "C" focus_status focus_decode_step(const focus_decode_desc* d, focus_stre
   return launch_step(d, p, d->workspace, reinterpret_cast<hipStream_t>(stream));
 }
 
+// ------------------------------------------------------- decode schedule
+
+namespace {
+
+// Cadence of window j of sequence b (a negative one raises BOUNDS, counts as 0).
+__device__ inline int sched_kmer(const focus_decode_sched& s, int b, int j) {
+  int k = s.kmer_uniform;
+  if (s.kmer) k = s.kmer[(int64_t)b * s.kmer_stride + min(max(j, 0), s.kmer_stride - 1)];
+  if (k < 0) {
+    focus::raise_err(s.err, FOCUS_ERR_BOUNDS);
+    k = 0;
+  }
+  return k;
+}
+
+// The insertion rule for one token of a sequence whose window j holds nw
+// bases with nk of them in the open k-mer: returns its FOCUS_STEP_* bits and
+// advances (j, nw, nk) past it.
+__device__ inline uint8_t sched_advance(const focus_decode_sched& s, int b, int& j, int& nw, int& nk) {
+  const int W = s.window_nt;
+  const int k = sched_kmer(s, b, j);
+  uint8_t kind = 0;
+  bool end;
+  if (k > 0 && (nk == k || (nw == W && nk > 0))) {
+    kind = FOCUS_STEP_SUMMARY;
+    nk = 0;
+    end = nw == W;
+  } else {
+    ++nw;
+    ++nk;
+    end = k == 0 && nw == W;
+  }
+  if (end) {
+    kind |= FOCUS_STEP_WINDOW_END;
+    ++j;
+    nw = 0;
+    nk = 0;
+  }
+  return kind;
+}
+
+// One thread per sequence.  start: walk tokens[b] tokens from the start of
+// window win_index[b]; otherwise derive the next token's kind.
+__global__ __launch_bounds__(256) void decode_sched(focus_decode_sched s, bool start) {
+  const int b = blockIdx.x * 256 + threadIdx.x;
+  if (b >= s.batch) return;
+  int j = s.win_index[b], nw, nk;
+  if (start) {
+    nw = nk = 0;
+    int summaries = 0;
+    const int n = max(s.tokens[b], 0);
+    for (int t = 0; t < n; ++t) summaries += sched_advance(s, b, j, nw, nk) & FOCUS_STEP_SUMMARY;
+    if (s.summaries) s.summaries[b] = summaries;
+  } else {
+    nw = s.bases_in_window[b];
+    nk = s.bases_in_kmer[b];
+    s.kind[b] = sched_advance(s, b, j, nw, nk);
+  }
+  s.win_index[b] = j;
+  s.bases_in_window[b] = nw;
+  s.bases_in_kmer[b] = nk;
+}
+
+focus_status launch_sched(const focus_decode_sched* s, bool start, focus_stream_t stream) {
+  if (!s) return FOCUS_E_NULL;
+  if (s->batch < 0 || s->window_nt < 1 || (!s->kmer && s->kmer_uniform < 0) || (s->kmer && s->kmer_stride < 1))
+    return FOCUS_E_ARG;
+  if (s->batch == 0) return FOCUS_OK;
+  if (!s->win_index || !s->bases_in_window || !s->bases_in_kmer || (start ? !s->tokens : !s->kind))
+    return FOCUS_E_NULL;
+  hipLaunchKernelGGL(decode_sched, dim3((uint32_t)focus::ceil_div(s->batch, 256)), dim3(256), 0,
+                     reinterpret_cast<hipStream_t>(stream), *s, start);
+  return focus::launch_status();
+}
+
+}  // namespace
+
+extern "C" focus_status focus_decode_sched_start(const focus_decode_sched* s, focus_stream_t stream) {
+  return launch_sched(s, true, stream);
+}
+
+extern "C" focus_status focus_decode_next_kind(const focus_decode_sched* s, focus_stream_t stream) {
+  return launch_sched(s, false, stream);
+}
+
 // ------------------------------------------------ allocation-free variant
 
 // The partials of focus_decode_step_noalloc live in this array: one copy per

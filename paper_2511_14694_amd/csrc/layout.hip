@@ -192,6 +192,13 @@ __global__ __launch_bounds__(kTokThreads) void layout_tokens(focus_layout_desc d
     else focus::raise_err(d.err, FOCUS_ERR_PLAN);
   }
   if (d.bases && d.token_ids) d.token_ids[tok] = summary ? d.summary_token_id : (int32_t)d.bases[base];
+  if (d.tok_next_base) {
+    // pi(t): the window's bases up to and including t, plus its first base
+    // (a summary follows the bases of its k-mer); -1 past the sequence's end
+    const int64_t end = d.win_base_off[d.cu_windows[b]] + d.seq_nt[b];
+    const int64_t nb = d.win_base_off[gw] + base_in_win + (summary ? 0 : 1);
+    d.tok_next_base[tok] = nb < end ? nb : -1;
+  }
 }
 
 }  // namespace

@@ -41,7 +41,7 @@ def test_struct_mirrors_and_version():
     for i, st in enumerate(_abi.STRUCTS):
         assert lib.focus_struct_size(i) == C.sizeof(st)
     assert lib.focus_struct_size(99) == -1
-    assert F.focus_abi_version() == 2
+    assert F.focus_abi_version() == 3
     assert lib.focus_status_str(0) == b"ok"
     assert lib.focus_status_str(5) == b"unsupported configuration"
 

@@ -201,6 +201,33 @@ def test_key_split_against_oracle(seq, H, Hkv, D, wins):
         assert torch.equal(o2[sl], p.o[sl]) and torch.equal(lse2[sl], p.lse[sl])
 
 
+def test_side_stream_scratch():
+    """A key-split launch on a side stream while the current stream keeps
+    allocating and writing: the call's scratch belongs to the side stream, so
+    the result equals the same launch on the current stream bit for bit."""
+    announce("attn key split on a side stream")
+    seq, W, H, D = [300_000], 1000, 2, 128
+    km = np.full(300, 100, np.int32)
+    p = Prefill(seq, W, km, H, 1, D, "bf16", seed=41, run=False)
+    ids = torch.tensor([299], dtype=torch.int32, device=DEV)
+    n = F.focus_window_attn_workspace(p.lay, p.q, p.k, p.v, p.ck, p.cv, ids)
+    assert n > 0
+    o_ref, lse_ref = p.attn(win_ids=ids)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    o = torch.zeros_like(o_ref)
+    lse = torch.zeros_like(lse_ref)
+    F.focus_window_attn(p.lay, p.q, p.k, p.v, p.ck, p.cv, o=o, lse=lse, win_ids=ids, stream=side)
+    # the current stream allocates blocks of the scratch's size and scribbles on them
+    junk = [torch.full((n,), 0xFF, dtype=torch.uint8, device=DEV) for _ in range(4)]
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    del junk
+    ref = build_layout(seq, W, km)
+    sl = slice(int(ref["win_tok_off"][299]), int(ref["win_tok_off"][299] + ref["win_ntok"][299]))
+    assert torch.equal(o[sl], o_ref[sl]) and torch.equal(lse[sl], lse_ref[sl])
+
+
 def test_window_subset_any_order_and_determinism():
     announce("attn window subset / determinism")
     seq, W = [5000], 1000

@@ -1,10 +1,12 @@
 """GPU parity of focus_decode_step against the oracle's streaming state machine
 (oracle.decode.DecodeSequence).
 
-The device side takes its step kinds from the device layout of one window
-(paper_2511_14694_amd.schedule); the oracle decides every token's kind itself.
-Both start from the same random cache/window contents and the same start
-position inside the window, and each derives its own initial lengths.
+The device derives every step's kind itself (DecodeSchedule:
+focus_decode_sched_start places each sequence part-way into its window,
+focus_decode_next_kind gives the next token's kind); the oracle decides every
+token's kind on its own.  Both start from the same random cache/window contents
+and the same start position inside the window, and each derives its own
+initial lengths.  Cadences are uniform or drawn per window.
 """
 
 import numpy as np
@@ -15,24 +17,28 @@ import focus_workloads as fw
 import paper_2511_14694_amd as F
 from gpu_util import DEV, announce, assert_parity, to64, torch_dtype
 from oracle.decode import DecodeSequence
-from paper_2511_14694_amd import schedule
 
 pytestmark = pytest.mark.gpu
 
 
 class DecodeRun:
+    """k: one cadence for every window, or [B, n] cadences of each sequence's
+    current window and the ones after it."""
+
     def __init__(self, B, H, Hkv, D, dtype, W, k, cache_rows0, starts, steps, seed,
                  split=0, cache_slack=None):
         self.B, self.H, self.Hkv, self.D, self.dtype = B, H, Hkv, D, dtype
         self.W, self.k, self.steps = W, k, steps
         self.starts = np.asarray(starts, np.int64)
         self.cache_rows0 = cache_rows0
-        # device layout of one full window -> step kinds and initial lengths
-        totals = F.focus_layout_plan([W], W, None, k)
-        lay = F.focus_layout(totals, [W], W, None, k)
-        self.win_kinds = lay["tok_kind"].cpu().numpy()
-        n0 = [schedule.initial_lengths(self.win_kinds, int(s)) for s in self.starts]
-        per_window = -(-W // k) if k else 0
+        # device schedule: place every sequence start[b] tokens into its window
+        uniform = np.ndim(k) == 0
+        self.sched = F.DecodeSchedule(B, W, None if uniform else np.asarray(k, np.int32),
+                                      int(k) if uniform else 0, device=DEV)
+        n_sum0 = self.sched.start(self.starts).clone()
+        n_base0 = self.sched.bases_in_window.clone()
+        kmin = int(k) if uniform else int(np.min(k))
+        per_window = -(-W // kmin) if kmin else 0
         slack = cache_slack if cache_slack is not None else per_window * (2 + steps // max(W, 1))
         self.cap_c = cache_rows0 + slack
         self.cap_w = W
@@ -47,10 +53,9 @@ class DecodeRun:
         self.sv = fw.randn((steps, B, Hkv, D), dtype, g + 7, DEV)
         self.init_k = (self.cache_k.clone(), self.win_k.clone())
         self.init_v = (self.cache_v.clone(), self.win_v.clone())
-        self.cache_len = torch.tensor([cache_rows0 + s for s, _ in n0], dtype=torch.int32, device=DEV)
-        self.win_len = torch.tensor([b for _, b in n0], dtype=torch.int32, device=DEV)
-        kinds = np.stack([schedule.step_kinds(self.win_kinds, int(s), steps) for s in self.starts], axis=1)
-        self.kinds = torch.as_tensor(kinds, device=DEV)                       # [steps, B]
+        self.cache_len = (n_sum0 + cache_rows0).to(torch.int32)
+        self.win_len = n_base0.clone()
+        self.kinds = torch.empty(steps, B, dtype=torch.uint8, device=DEV)     # [steps, B], as derived
         self.o = torch.empty(steps, B, H, D, dtype=td, device=DEV)
         self.lse = torch.empty(steps, B, H, dtype=torch.float32, device=DEV)
         self.len_hist = torch.empty(steps, 2, B, dtype=torch.int32, device=DEV)
@@ -58,7 +63,8 @@ class DecodeRun:
         ws = F.focus_decode_workspace(self.sq[0], self.sk[0], self.cache_k, self.win_k, split)
         self.ws = torch.empty(ws, dtype=torch.uint8, device=DEV)
         for i in range(steps):
-            F.focus_decode_step(self.sq[i], self.sk[i], self.sv[i], self.kinds[i], self.cache_k, self.cache_v,
+            self.kinds[i].copy_(self.sched.next_kind())
+            F.focus_decode_step(self.sq[i], self.sk[i], self.sv[i], self.sched.kind, self.cache_k, self.cache_v,
                                 self.cache_len, self.win_k, self.win_v, self.win_len, o=self.o[i],
                                 lse=self.lse[i], workspace=self.ws, split_keys=split, err=self.err)
             self.len_hist[i, 0].copy_(self.cache_len)
@@ -67,13 +73,15 @@ class DecodeRun:
 
     def oracle(self, b, sample_steps):
         """Run the oracle over every step of sequence b; compare at sample_steps."""
-        n_bases, n_sum, open_kmer = DecodeSequence.replay_counters(self.W, self.k, int(self.starts[b]))
+        k_b = self.k if np.ndim(self.k) == 0 else [int(x) for x in self.k[b]]
+        n_bases, n_sum, open_kmer = DecodeSequence.replay_counters(
+            self.W, k_b if np.ndim(k_b) == 0 else k_b[0], int(self.starts[b]))
         c0 = self.cache_rows0 + n_sum
         ck = to64(self.init_k[0][b, :c0]).astype(np.float32)
         cv = to64(self.init_v[0][b, :c0]).astype(np.float32)
         wk = to64(self.init_k[1][b, :n_bases]).astype(np.float32)
         wv = to64(self.init_v[1][b, :n_bases]).astype(np.float32)
-        st = DecodeSequence(self.W, self.k, ck, cv, wk, wv, n_bases, open_kmer)
+        st = DecodeSequence(self.W, k_b, ck, cv, wk, wv, n_bases, open_kmer)
         q = to64(self.sq[:, b])
         k = to64(self.sk[:, b]).astype(np.float32)
         v = to64(self.sv[:, b]).astype(np.float32)
@@ -98,6 +106,39 @@ def test_decode_small_every_step(dtype, D, Hkv):
                   starts=[1, 17, 45], steps=70, seed=300 + D)
     assert int(r.err.item()) == 0
     for b in range(3):
+        r.oracle(b, set(range(70)))
+
+
+def test_decode_per_window_cadence():
+    """Every window draws its own cadence from {50, 100, 200, 500} (the ragged
+    schedule): the device schedule switches cadence at each window end, and
+    every step matches the oracle, which switches on its own."""
+    announce("decode per-window cadence")
+    B, W, steps = 4, 1000, 2600
+    rng = np.random.default_rng(11)
+    km = rng.choice([50, 100, 200, 500], (B, 4)).astype(np.int32)
+    starts = rng.integers(1, 900, B)
+    r = DecodeRun(B=B, H=4, Hkv=2, D=128, dtype="bf16", W=W, k=km, cache_rows0=40, starts=starts,
+                  steps=steps, seed=19)
+    assert int(r.err.item()) == 0
+    kinds = r.kinds.cpu().numpy()
+    assert ((kinds & F.FOCUS_STEP_WINDOW_END) > 0).sum(0).min() >= 2    # every sequence crosses two windows
+    for b in range(B):
+        ends = np.nonzero(kinds[:, b] & F.FOCUS_STEP_WINDOW_END)[0]
+        sample = set(range(0, steps, 97)) | {int(e) for e in ends} | {int(e) + 1 for e in ends}
+        r.oracle(b, {i for i in sample if i < steps})
+
+
+def test_decode_mixed_cadences_every_step():
+    """Small windows whose cadences include k = 0 (no summaries: the window
+    ends at its W-th base) and k = W (one summary per window); every step
+    against the oracle."""
+    announce("decode mixed cadences")
+    km = np.array([[0, 5, 3, 0, 12, 1], [4, 0, 12, 1, 0, 5]], np.int32)
+    r = DecodeRun(B=2, H=4, Hkv=2, D=64, dtype="bf16", W=12, k=km, cache_rows0=9, starts=[3, 0],
+                  steps=70, seed=23, cache_slack=70)
+    assert int(r.err.item()) == 0
+    for b in range(2):
         r.oracle(b, set(range(70)))
 
 

@@ -2,7 +2,8 @@
 compared bit for bit with the oracle (oracle.layout, oracle.attention.compact)
 on random small batches (ragged lengths, empty sequences, k = 0 windows, a
 partial last window and k-mer), the hand-worked examples, and every workload
-at its full size."""
+at its full size.  The optional target map pi(t) (tok_next_base) is part of
+every comparison."""
 
 import numpy as np
 import pytest
@@ -17,7 +18,7 @@ pytestmark = pytest.mark.gpu
 
 FIELDS = ["cu_windows", "cu_tokens", "cu_summaries", "win_seq", "win_nt", "win_nsum", "win_ntok",
           "win_tok_off", "win_cache_off", "win_sum_off", "win_base_off", "tok_pos", "tok_kind",
-          "tok_base", "tok_kmer", "tok_win", "sum_tok"]
+          "tok_base", "tok_kmer", "tok_win", "sum_tok", "tok_next_base"]
 SID = 260   # the reserved summary token id (outside the byte range of bases)
 
 
@@ -25,7 +26,7 @@ def run_layout(seq, W, kmer, with_bases=True):
     totals = F.focus_layout_plan(seq, W, kmer)
     bases = fw.random_bases(int(sum(seq)), 7) if with_bases else None
     err = torch.zeros(1, dtype=torch.int32, device=DEV)
-    lay = F.focus_layout(totals, seq, W, kmer, bases=bases, summary_token_id=SID, err=err)
+    lay = F.focus_layout(totals, seq, W, kmer, bases=bases, summary_token_id=SID, err=err, next_base=True)
     torch.cuda.synchronize()
     return lay, bases, int(err.item())
 
