@@ -100,6 +100,68 @@ class Timer:
         return float(np.mean(xs)) if xs else float("nan")
 
 
+class ClockSampler:
+    """Samples the GPU's graphics clock (mean over its XCDs, MHz) and socket
+    power (W) every few ms while the timed steps run, through amdsmi's GPU
+    metrics; reports nothing when amdsmi is unavailable."""
+
+    def __init__(self, period_s=0.005):
+        import threading
+        self.period = period_s
+        self.samples = []
+        self.error = None
+        self.ok = False
+        self._stop = threading.Event()
+        self._thread = None
+        try:
+            import amdsmi
+            amdsmi.amdsmi_init()
+            self._smi = amdsmi
+            self._h = amdsmi.amdsmi_get_processor_handles()[0]
+            self.ok = True
+        except Exception as e:
+            self.ok = False
+            self.error = repr(e)
+
+    def _read(self):
+        m = self._smi.amdsmi_get_gpu_metrics_info(self._h)
+        clks = [c for c in m.get("current_gfxclks", []) if isinstance(c, (int, float)) and c < 0xFFFF]
+        clk = float(np.mean(clks)) if clks else float(m.get("current_gfxclk", float("nan")))
+        pw = m.get("current_socket_power", float("nan"))
+        return clk, float(pw) if isinstance(pw, (int, float)) else float("nan")
+
+    def __enter__(self):
+        import threading
+        if self.ok:
+            def loop():
+                while not self._stop.is_set():
+                    try:
+                        self.samples.append(self._read())
+                    except Exception as e:
+                        self.error = repr(e)
+                    time.sleep(self.period)
+            self._thread = threading.Thread(target=loop, daemon=True)
+            self._thread.start()
+        return self
+
+    def __exit__(self, *a):
+        self._stop.set()
+        if self._thread:
+            self._thread.join()
+        return False
+
+    def summary(self):
+        # samples taken while the clock is up (the GPU busy), not idle ones
+        busy = [c for c in self.samples if c[0] > 500]
+        if not self.ok or not busy:
+            return {"unavailable": self.error or f"{len(self.samples)} samples, none with the clock up"}
+        clk = np.array([c[0] for c in busy])
+        pw = np.array([c[1] for c in busy])
+        return {"gfxclk_MHz_mean": float(clk.mean()), "gfxclk_MHz_min": float(clk.min()),
+                "socket_power_W_mean": float(np.nanmean(pw)) if np.isfinite(pw).any() else None,
+                "samples": len(busy), "source": "amdsmi GPU metrics (current_gfxclks, current_socket_power)"}
+
+
 def prefill_setup(torch, F, fw, w):
     dev = torch.device("cuda:0")
     seq = [w.seq_nt] * w.batch
@@ -144,17 +206,156 @@ def prefill_step(torch, F, s, timer=None):
         a[1].record()
 
 
+def kv_bytes(w, totals):
+    """Retained summary K/V against the K/V a dense decoder keeps for the same
+    bases, per attention layer, all sequences (the memory the paper's scaling
+    curves measure; eq. kv-budget / kv-ratio)."""
+    elt = 2 if w.dtype == "bf16" else 4
+    row = 2 * w.kv_heads * w.head_dim * elt            # K and V of one token
+    summary = totals.n_summaries * row
+    dense = w.seq_nt * w.batch * row
+    return {"summary_kv_bytes": summary, "dense_kv_bytes": dense, "ratio": summary / dense}
+
+
+def secondary_prefill_config(torch, F, fw, name, reps=5):
+    """Another prefill configuration, attention only: masked-parallel (every
+    window of every sequence in one launch) and streaming (window j of every
+    sequence in one call, j = 0, 1, ...), against the bf16 MFMA peak with the
+    visible pairs of the drawn layout; plus the summary-KV / dense-KV bytes."""
+    w = fw.WORKLOADS[name]
+    s = prefill_setup(torch, F, fw, w)
+    prefill_step(torch, F, s)          # layout + compaction fill the cache
+    timer = Timer(torch)
+    for _ in range(reps):
+        a = timer.span("mp")
+        a[0].record()
+        F.focus_window_attn(s["lay"], s["q"], s["k"], s["v"], s["ck"], s["cv"], o=s["o"], lse=s["lse"])
+        a[1].record()
+    torch.cuda.synchronize()
+    ms = timer.mean_ms("mp")
+    lay = s["lay"]
+    pairs = visible_pairs(lay["win_ntok"].cpu().numpy(), lay["win_cache_off"].cpu().numpy())
+    flops = 4 * w.head_dim * w.heads * pairs
+    # streaming: every sequence's window j per call (the batch advances in step)
+    nw = fw.windows_per_seq(w.seq_nt, w.window_nt)
+    cu = lay["cu_windows"].cpu().numpy()
+    ids = [torch.tensor([int(cu[b]) + j for b in range(w.batch) if int(cu[b]) + j < int(cu[b + 1])],
+                        dtype=torch.int32, device="cuda:0") for j in range(nw)]
+    n_ws = max(F.focus_window_attn_workspace(lay, s["q"], s["k"], s["v"], s["ck"], s["cv"], i) for i in ids)
+    ws = torch.empty(max(n_ws, 16), dtype=torch.uint8, device="cuda:0")
+
+    def stream_pass():
+        for i in ids:
+            F.focus_window_attn(lay, s["q"], s["k"], s["v"], s["ck"], s["cv"], o=s["o"], lse=s["lse"],
+                                win_ids=i, workspace=ws)
+
+    stream_pass()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    stream_pass()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_stream = e0.elapsed_time(e1)
+    nt = w.seq_nt * w.batch
+    out = {"workload": f"{w.name}: batch {w.batch} x {w.seq_nt:,} nt, windows of {w.window_nt} nt, "
+                       + (f"one summary per {w.kmer} nt" if w.kmer else
+                          f"cadence per window drawn from {list(w.kmer_choices)}")
+                       + f", {w.heads} x {w.head_dim} {w.dtype}",
+           "visible_pairs_per_head": pairs, "flops": flops,
+           "masked_parallel": {"ms": ms, "nt_per_s": nt / (ms * 1e-3), "tflops": flops / ms / 1e9,
+                               "frac_mfma": flops / (ms * 1e-3) / PEAK_BF16_FLOPS},
+           "streaming": {"calls": nw, "windows_per_call": w.batch, "ms": ms_stream,
+                         "nt_per_s": nt / (ms_stream * 1e-3), "frac_mfma": flops / (ms_stream * 1e-3) / PEAK_BF16_FLOPS,
+                         "workspace_bytes": n_ws},
+           "kv_bytes_per_layer": kv_bytes(w, s["totals"])}
+    del s, ws
+    torch.cuda.empty_cache()
+    return out
+
+
+def cpu_baseline_decode(budget_s=12.0):
+    """The decode oracle as it stands on the batch-16 ~1 Mb decode workload:
+    for every sequence, the states at steps 1, 2, 3, the first summary step,
+    the first window end and the last step (lengths from the oracle's own
+    replay of the layout rule, random K/V rows of those lengths), one oracle
+    step's attention each, until the time budget is used; the 1000-step run is
+    extrapolated by the keys read."""
+    import focus_workloads as fw
+    from oracle.decode import DecodeSequence
+    w = fw.WORKLOADS["decode_b16_1mb"]
+    W, k, steps, H, Hkv, D = w.window_nt, w.kmer, w.decode_steps, w.heads, w.kv_heads, w.head_dim
+    starts = fw.decode_positions(w)
+    rng = np.random.default_rng(fw.BASE_SEED)
+    cores = len(os.sched_getaffinity(0))
+    try:
+        from threadpoolctl import threadpool_limits
+        limiter = threadpool_limits(limits=cores)
+    except Exception:
+        limiter = None
+    samples, total_keys = [], 0
+    z = np.zeros((1, 1), np.float32)
+    for b in range(w.batch):
+        nb, ns, ok = DecodeSequence.replay_counters(W, k, int(starts[b]))
+        st = DecodeSequence(W, k, [z] * (w.decode_cache_rows + ns), [z] * (w.decode_cache_rows + ns),
+                            [z] * nb, [z] * nb, nb, ok)
+        lens, first_s, first_e = [], None, None
+        for i in range(steps):
+            _, _, kind, end = st.step(None, z, z, compute=False)
+            lens.append((st.cache_len, st.win_len if not end else st.win_len))
+            if kind == 1 and first_s is None:
+                first_s = i
+            if end and first_e is None:
+                first_e = i
+        # keys the step attends over: the lengths right after its append
+        keys = [c + wl for c, wl in lens]
+        total_keys += sum(keys)
+        for i in sorted({0, 1, 2, first_s or 0, first_e or 0, steps - 1}):
+            samples.append((b, i, keys[i]))
+    done_keys, t = 0, 0.0
+    nmax = max(nk for _, _, nk in samples)
+    pool_k = rng.standard_normal((nmax, Hkv, D)).astype(np.float32)
+    pool_v = rng.standard_normal((nmax, Hkv, D)).astype(np.float32)
+    for b, i, nk in samples:
+        st = DecodeSequence(W, k, list(pool_k[:nk]), list(pool_v[:nk]), [], [], 0, 0)
+        q = rng.standard_normal((H, D))
+        c0 = time.perf_counter()
+        st.attend(q)
+        t += time.perf_counter() - c0
+        done_keys += nk
+        if t > budget_s:
+            break
+    if limiter is not None:
+        limiter.restore_original_limits()
+    t_full = t * total_keys / done_keys
+    return {"value": w.batch * steps / t_full, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": (f"oracle decode attention at {len(samples)} sampled (sequence, step) states of "
+                       f"decode_b16_1mb (steps 1, 2, 3, first summary, first window end, {steps}), "
+                       f"{done_keys:,} of {total_keys:,} keys in {t:.1f} s; the {steps}-step run "
+                       f"extrapolated by keys to {t_full:.0f} s")}
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(torch, s, budget_s=20.0):
     """The oracle, as it is, on whole windows of the same workload (all heads):
     the last window first, then earlier ones, until the time budget is used.
     The full-workload time is extrapolated by the visible-pair ratio."""
     from oracle import attention as A
     from oracle.layout import build_layout
+    cores = len(os.sched_getaffinity(0))
     try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        from threadpoolctl import threadpool_limits
+        limiter = threadpool_limits(limits=cores)     # BLAS threads = the host cores this process may use
     except Exception:
-        cores = len(os.sched_getaffinity(0))
+        limiter = None
     w = s["w"]
     t_layout0 = time.perf_counter()
     ref = build_layout([w.seq_nt] * w.batch, w.window_nt, fw_kmer(w))
@@ -180,7 +381,10 @@ def cpu_baseline(torch, s, budget_s=20.0):
             break
     total_pairs = visible_pairs(ref["win_ntok"], ref["win_cache_off"])
     t_full = t_attn * total_pairs / pairs + t_layout
+    if limiter is not None:
+        limiter.restore_original_limits()
     return {"value": w.seq_nt * w.batch / t_full, "unit": "nt/s", "cores": int(cores), "kind": "oracle",
+            "cpu_model": cpu_model(),
             "sample": (f"oracle window attention on {len(done)} windows {_span(done)} (all {w.heads} heads, "
                        f"{pairs:,} of {total_pairs:,} visible pairs per head) in {t_attn:.1f} s, "
                        f"plus the full oracle layout walk ({t_layout:.1f} s); full-workload time "
@@ -549,11 +753,13 @@ def main():
     timer = Timer(torch)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    e0.record()
-    for i in range(args.steps):
-        prefill_step(torch, F, s, timer)
-    e1.record()
-    torch.cuda.synchronize()
+    clock = ClockSampler()
+    with clock:
+        e0.record()
+        for i in range(args.steps):
+            prefill_step(torch, F, s, timer)
+        e1.record()
+        torch.cuda.synchronize()
     total_ms = e0.elapsed_time(e1)
     ms_step = total_ms / max(args.steps, 1)
     log(f"timed {args.steps} steps: {ms_step:.3f} ms/step")
@@ -589,6 +795,8 @@ def main():
         "kernel_ms": {"layout": timer.mean_ms("layout"), "compact": timer.mean_ms("compact"),
                       "attn": attn_ms},
         "augmented_tokens_per_s": s["totals"].n_tokens / (ms_step * 1e-3),
+        "clock_under_load": clock.summary(),
+        "kv_bytes_per_layer": kv_bytes(w, s["totals"]),
     }
     if not args.no_secondary:
         log("secondary: compaction")
@@ -602,11 +810,16 @@ def main():
         if not args.no_cpu_baseline:
             log("cpu baseline (oracle)")
             result["cpu_baseline"] = cpu_baseline(torch, s, args.cpu_budget)
+            log("cpu baseline (decode oracle)")
+            result["cpu_baseline"]["decode"] = cpu_baseline_decode()
         del s
         torch.cuda.empty_cache()
         log("secondary: decode")
         sec["decode_b16_1mb"] = secondary_decode(torch, F, fw)
         torch.cuda.empty_cache()
+        for name in ("prefill_100kb", "ragged_b8_256kb"):
+            log(f"secondary: {name}")
+            sec[name] = secondary_prefill_config(torch, F, fw, name)
         log("secondary: dense 32 kb")
         sec["dense_32kb"] = secondary_dense(torch, F, fw)
         torch.cuda.empty_cache()
