@@ -39,8 +39,8 @@
 // two-stage form of the same MFMA scheme: 4 waves, each copying its share.
 //
 // Summary queries (the FOCUS adapter's attention): under C(t) several windows'
-// summaries share one wave (attn_sq_group); otherwise the bf16 kernel above
-// runs with one wave of 32 summary slots per (window, head).
+// summaries share one workgroup (attn_sq_block); otherwise the bf16 kernel
+// above runs with one wave of 32 summary slots per (window, head).
 //
 // f32 path: a plain VALU kernel (4 lanes per query row, exact online softmax),
 // used for the float32 checks; it is not tuned.
@@ -904,31 +904,54 @@ __global__ __launch_bounds__(512, 2) void attn_ct(
 
 // --------------------------------------- bf16 MFMA, summary queries under C(t)
 
-// The adapter attention under C(t) with several windows per wave: G listed
-// windows in a row (list entries G gi .. G gi + G - 1) put their summaries in
-// the wave's 32 query slots (window k's B_k summaries at slots off_k ..
-// off_k + B_k - 1, off_k = B_0 + ... + B_{k-1}).  A pass covers a run of the
-// group's windows on one sequence: that sequence's cache rows [0, max C) once,
-// a row visible to a slot while it is below the slot's own window's C_w (the
-// caches of consecutive windows are prefixes of each other), then each
-// window's rows [0, its last summary's row], visible to that window's slots up
-// to the slot's own row.  So the cache prefix is streamed once for G windows,
-// and 32 slots hold G B_w queries instead of B_w.  Keys move in 32-row tiles
-// through two LDS stages (32 KB: five workgroups of one wave per CU).
-template <int D>
-__global__ __launch_bounds__(64) void attn_sq_group(focus_attn_desc d, float sc, int64_t n_pairs, int64_t nwl, int G,
-                                                    SumQ sq) {
+// The adapter attention under C(t) (eq. focus-attn with the summary tokens as
+// the only queries), many windows per workgroup: G listed windows in a row put
+// their summaries in the workgroup's 32 W query slots (window k's B_k
+// summaries at slots off_k .. off_k + B_k - 1, off_k = B_0 + ... + B_{k-1};
+// wave w holds slots 32 w .. 32 w + 31).  For each run of the group's windows
+// on one sequence:
+//   cache phase   the W waves stream that sequence's cache rows [0, max C)
+//                 once, in 64-row stages through two shared LDS stages, every
+//                 wave copying its share and a barrier closing each stage; a
+//                 row is visible to a slot while it is below the C_w of the
+//                 slot's own window (the caches of the windows of one sequence
+//                 are prefixes of each other), so the cache crosses into LDS
+//                 once per 32 W slots instead of once per window;
+//   window phase  each wave, on its own, streams rows [0, last summary's row]
+//                 of each window it holds slots of, 32 rows at a time through
+//                 its private LDS region, visible to that window's slots up to
+//                 the slot's own row.  A tile's operands go to registers
+//                 before the next tile is copied into the same region, so the
+//                 copy overlaps the tile's arithmetic.
+// Every summary of a window must see the window's rows up to its own, and the
+// last summary ends the window: the window phase reads essentially every K/V
+// row once, which bounds the kernel by HBM.  A slot that holds no summary has a
+// zero query and sees every key (its result is dropped), so it forces no
+// masking.
+template <int D, int W>
+__global__ __launch_bounds__(64 * W, 2) void attn_sq_block(focus_attn_desc d, float sc, int64_t n_pairs, int64_t nwl,
+                                                          int G, int wpw, SumQ sq) {
+  static_assert(W == 4 || W == 8, "four or eight waves");
+  constexpr int kSlots = 32 * W;
   constexpr int kBK = 32, kRB = D * 2, kTile = kBK * kRB, kCh16 = kRB / 16;
   constexpr int kKsteps = D / 16, kDtiles = D / 32;
-  constexpr int kDma = kTile / 1024;  // wave copies per tile and tensor
-  constexpr int kRPK = 1024 / kRB;    // tile rows per wave copy
-  __shared__ __attribute__((aligned(1024))) char kbuf0[kTile], kbuf1[kTile];
-  __shared__ __attribute__((aligned(1024))) char vbuf0[kTile], vbuf1[kTile];
-  // per window of the group: window id, T, C_w, sequence, summaries, slot offset
-  __shared__ int64_t wg_win[32], wg_tok0[32], wg_s0[32];
-  __shared__ int wg_C[32], wg_b[32], wg_ns[32], wg_off[32], wg_nwk[32];
+  constexpr int kRPK = 1024 / kRB;             // rows per 1 KB wave copy
+  constexpr int kTileCopies = kTile / 1024;    // wave copies per 32-row tile and tensor
+  constexpr int kStage = 2 * kTile;            // a 64-row stage of one tensor = one region
+  constexpr int kStageCopies = kStage / 1024;
+  constexpr int kUnused = W == 8 ? 2 * kTile : 16;
+  // one region per wave: [K tile | V tile] in the window phase; in the cache
+  // phase regions 0 / 1 are K / V of stage 0 and regions 2 / 3 of stage 1
+  __shared__ __attribute__((aligned(1024))) char rg0[2 * kTile], rg1[2 * kTile], rg2[2 * kTile], rg3[2 * kTile];
+  __shared__ __attribute__((aligned(1024))) char rg4[kUnused], rg5[kUnused], rg6[kUnused], rg7[kUnused];
+  // per window of the group: token and summary offsets, window id, C_w,
+  // sequence, summaries, slot offset, rows of the window phase
+  __shared__ int64_t wg_tok0[kSlots], wg_s0[kSlots];
+  __shared__ int wg_win[kSlots], wg_C[kSlots], wg_b[kSlots], wg_ns[kSlots], wg_off[kSlots + 1], wg_nwk[kSlots];
+  __shared__ int bad_any;
 
-  const int lane = threadIdx.x, l32 = lane & 31, g = lane >> 5;
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, l32 = lane & 31, g = lane >> 5;
   const Item it = map_block(blockIdx.x, n_pairs, d.n_heads, 1);
   if (!it.valid) return;
   const int H = d.n_heads, Hkv = d.n_kv_heads, h = it.h;
@@ -937,84 +960,117 @@ __global__ __launch_bounds__(64) void attn_sq_group(focus_attn_desc d, float sc,
   const int nk = (int)min((int64_t)G, nwl - li0);  // windows in this group
   if (nk <= 0) return;
 
-  // lane k < nk reads window k's description; slot offsets by a prefix sum
-  bool bad = false;
-  if (lane < nk) {
-    const int64_t gw = listed_window(d, li0 + lane);
-    if (gw < 0 || gw >= d.totals.n_windows) {
-      bad = true;
-    } else {
+  // thread k < nk reads window k's description; slot offsets by a prefix sum
+  if (tid == 0) bad_any = 0;
+  __syncthreads();
+  if (tid < nk) {
+    const int64_t gw = listed_window(d, li0 + tid);
+    bool bad = gw < 0 || gw >= d.totals.n_windows;
+    if (!bad) {
       const int T = d.win_ntok[gw], C = d.win_cache_off[gw], b = d.win_seq[gw], ns = sq.win_nsum[gw];
       const int64_t tok0 = d.win_tok_off[gw] - d.qkv_tok_base, s0 = sq.win_sum_off[gw];
       bad = b < 0 || b >= d.batch || C < 0 || C > d.cache_cap || tok0 < 0 || tok0 + T > d.qkv_rows || ns < 0 ||
             ns > T || s0 < sq.base || s0 + ns > sq.base + sq.rows;
       if (!bad) {
-        wg_win[lane] = gw;
-        wg_tok0[lane] = tok0;
-        wg_s0[lane] = s0;
-        wg_C[lane] = C;
-        wg_b[lane] = b;
-        wg_ns[lane] = ns;
-        // keys of the window phase: rows up to the last summary's
+        wg_win[tid] = (int)gw;
+        wg_tok0[tid] = tok0;
+        wg_s0[tid] = s0;
+        wg_C[tid] = C;
+        wg_b[tid] = b;
+        wg_ns[tid] = ns;
         int nwk = 0;
         if (ns > 0) {
           const int64_t r = sq.sum_tok[s0 + ns - 1] - d.win_tok_off[gw];
           nwk = (int)(r < 0 ? 0 : r >= T ? T - 1 : r) + 1;
         }
-        wg_nwk[lane] = nwk;
+        wg_nwk[tid] = nwk;
       }
     }
-  }
-  if (__any(bad)) {
-    if (lane == 0) focus::raise_err(d.err, FOCUS_ERR_BOUNDS);
-    return;
-  }
-  if (lane == 0) {
-    int off = 0;
-    for (int k = 0; k < nk; ++k) {
-      wg_off[k] = off;
-      off += wg_ns[k];
-    }
-    if (off > 32) focus::raise_err(d.err, FOCUS_ERR_BOUNDS);  // more summaries than slots
+    if (bad) bad_any = 1;
   }
   __syncthreads();
+  if (tid == 0 && !bad_any) {
+    // wpw > 0: wpw whole windows per wave (window k opens wave k / wpw at its
+    // first slot), so that no window's rows are streamed by two waves;
+    // wpw = 0: the summaries packed one after the other
+    int off = 0;
+    for (int k = 0; k < nk; ++k) {
+      if (wpw > 0 && k % wpw == 0) off = 32 * (k / wpw);
+      wg_off[k] = off;
+      off += wg_ns[k];
+      if (wpw > 0 && off > 32 * (k / wpw + 1)) bad_any = 1;  // a window past its wave's slots
+    }
+    wg_off[nk] = off;
+    if (off > kSlots) bad_any = 1;  // more summaries than slots
+  }
+  __syncthreads();
+  if (bad_any) {
+    if (tid == 0) focus::raise_err(d.err, FOCUS_ERR_BOUNDS);
+    return;
+  }
 
-  // this lane's slot: window kl, its summary (global index s), window row pos
+  // this lane's slot: window kl (the last window whose offset is <= slot),
+  // its summary s (global index) and the summary's window row pos
+  const int slot = wave * 32 + l32;
   int kl = -1, pos = 0;
   int64_t s = 0;
-  for (int k = 0; k < nk; ++k)
-    if (l32 >= wg_off[k] && l32 < wg_off[k] + wg_ns[k]) kl = k;
+  if (slot < wg_off[nk]) {
+    int lo = 0, hi = nk - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (wg_off[mid] <= slot) lo = mid; else hi = mid - 1;
+    }
+    kl = slot - wg_off[lo] < wg_ns[lo] ? lo : -1;  // else a slot between two waves' windows
+  }
   if (kl >= 0) {
-    s = wg_s0[kl] + (l32 - wg_off[kl]);
+    s = wg_s0[kl] + (slot - wg_off[kl]);
     const int64_t r = sq.sum_tok[s] - d.win_tok_off[wg_win[kl]];
     pos = (int)min(max(r, (int64_t)0), (int64_t)wg_nwk[kl] - 1);
   }
   const int Cl = kl >= 0 ? wg_C[kl] : 0;
-  // an unused slot (its result is dropped) sees every key of every phase, so
-  // it forces no masking
   constexpr int kAll = 1 << 30;
+  // the windows this wave holds slots of: [kw_lo, kw_hi]
+  int kw_lo = kl < 0 ? kAll : kl, kw_hi = kl;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    kw_lo = min(kw_lo, __shfl_xor(kw_lo, o));
+    kw_hi = max(kw_hi, __shfl_xor(kw_hi, o));
+  }
+  kw_lo = __builtin_amdgcn_readfirstlane(kw_lo);
+  kw_hi = __builtin_amdgcn_readfirstlane(kw_hi);
 
-  // Q^T as the B operand: lane holds slot l32, head_dim [16 s + 8 g, +8)
+  // Q^T as the B operand: lane holds slot l32, head_dim [16 k + 8 g, +8)
   bf16x8 qf[kKsteps];
-  {
-    const int64_t qrow = (kl >= 0 ? s : wg_s0[0]) - sq.base;
+#pragma unroll
+  for (int k = 0; k < kKsteps; ++k)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) qf[k][e] = (__bf16)0.f;
+  if (kl >= 0) {
     const bf16x8* qp =
-        reinterpret_cast<const bf16x8*>(reinterpret_cast<const __bf16*>(sq.q) + (qrow * H + h) * D);
+        reinterpret_cast<const bf16x8*>(reinterpret_cast<const __bf16*>(sq.q) + ((s - sq.base) * H + h) * D);
 #pragma unroll
     for (int k = 0; k < kKsteps; ++k) qf[k] = qp[2 * k + g];
   }
 
   const uint32_t row_bytes = (uint32_t)(Hkv * D * 2);
-  uint32_t rowb[kDma], kchunk[kDma], vchunk[kDma];
-#pragma unroll
-  for (int i = 0; i < kDma; ++i) {
+  // wave copy i of a run of rows starting at row0 (nvalid rows real, the rest
+  // repeat the last one): rows i kRPK + lane / kCh16, swizzled as k_off / v_off
+  // lay them out, into K at kt and V at vt
+  auto copy_one = [&](const char* kbase, const char* vbase, int row0, int nvalid, char* kt, char* vt, int i)
+      __attribute__((always_inline)) {
     const int r = i * kRPK + lane / kCh16;
     const int p = lane % kCh16;
     const int f = D == 128 ? (r & 3) : ((r >> 1) & 1);
-    rowb[i] = (uint32_t)r * row_bytes;
-    kchunk[i] = (uint32_t)((p ^ (r % kCh16)) * 16);
-    vchunk[i] = (uint32_t)((((p >> 2) ^ f) * 4 + (p & 3)) * 16);
-  }
+    const uint32_t rb = (uint32_t)min(r, nvalid - 1 - row0) * row_bytes;
+    const char* kb = kbase + (int64_t)row0 * row_bytes;
+    const char* vb = vbase + (int64_t)row0 * row_bytes;
+    const char* ks = kb + (rb + (uint32_t)((p ^ (r % kCh16)) * 16));
+    const char* vs = vb + (rb + (uint32_t)((((p >> 2) ^ f) * 4 + (p & 3)) * 16));
+    char* kd = kt + i * 1024;
+    char* vd = vt + i * 1024;
+    __builtin_amdgcn_global_load_lds(ks, (lds_void*)kd, 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(vs, (lds_void*)vd, 16, 0, 0);
+  };
 
   f32x16 oacc[kDtiles];
 #pragma unroll
@@ -1024,30 +1080,42 @@ __global__ __launch_bounds__(64) void attn_sq_group(focus_attn_desc d, float sc,
   float m_run = kMinit, l_run = 0.f;
   const int grp = lane >> 4, ri = (lane >> 2) & 3, bq = lane & 3;
 
-  // rows [row0, row0 + 32) of the K/V rows at (kbase, vbase), nvalid of them
-  // real (the rest repeat the last one and are masked)
-  auto issue = [&](const char* kbase, const char* vbase, int row0, int nvalid, char* kt, char* vt) __attribute__((always_inline)) {
-    const uint32_t last = (uint32_t)(nvalid - 1 - row0) * row_bytes;
-    const char* kb = kbase + (int64_t)row0 * row_bytes;
-    const char* vb = vbase + (int64_t)row0 * row_bytes;
+  // operands of one 32-row tile (K at kt, V at vt) into registers.  The
+  // per-lane LDS offsets are computed once and kept opaque, so that every read
+  // is a base, this offset and an immediate (V rows 16 m + 8 hi only add a
+  // constant: the swizzle of v_off depends on the row mod 4).
+  int kofs[kKsteps], vofs[kDtiles];
 #pragma unroll
-    for (int i = 0; i < kDma; ++i) {
-      const uint32_t rb = nvalid - row0 >= kBK ? rowb[i] : min(rowb[i], last);
-      const char* ks = kb + (rb + kchunk[i]);
-      const char* vs = vb + (rb + vchunk[i]);
-      __builtin_amdgcn_global_load_lds(ks, (lds_void*)(kt + i * 1024), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(vs, (lds_void*)(vt + i * 1024), 16, 0, 0);
-    }
+  for (int k = 0; k < kKsteps; ++k) {
+    kofs[k] = k_off<D>(l32, 2 * k + g);
+    asm volatile("" : "+v"(kofs[k]));
+  }
+#pragma unroll
+  for (int dt = 0; dt < kDtiles; ++dt) {
+    vofs[dt] = v_off<D>(4 * (grp >> 1) + ri, 2 * (32 * dt + 16 * (grp & 1) + 4 * bq));
+    asm volatile("" : "+v"(vofs[dt]));
+  }
+  bf16x8 kop[kKsteps], vop[2 * kDtiles];
+  auto read_ops = [&](const char* kt, const char* vt) __attribute__((always_inline)) {
+#pragma unroll
+    for (int k = 0; k < kKsteps; ++k) kop[k] = *reinterpret_cast<const bf16x8*>(kt + kofs[k]);
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+#pragma unroll
+      for (int dt = 0; dt < kDtiles; ++dt) {
+        // keys of B slot v: 16 m + 8 (v/4) + 4 g + v%4
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vt + vofs[dt] + 16 * m * kRB));
+        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vt + vofs[dt] + (16 * m + 8) * kRB));
+        vop[m * kDtiles + dt] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      }
   };
-  // one 32-key tile: tile key kk is visible to this lane iff kk <= lim
-  auto compute = [&](const char* kt, const char* vt, int lim, bool need_mask) __attribute__((always_inline)) {
+  // one tile from the registers: tile key kk is visible to this lane iff kk <= lim
+  auto compute = [&](int lim, bool need_mask) __attribute__((always_inline)) {
     f32x16 sacc;
 #pragma unroll
     for (int v = 0; v < 16; ++v) sacc[v] = 0.f;
 #pragma unroll
-    for (int k = 0; k < kKsteps; ++k)
-      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(kt + k_off<D>(l32, 2 * k + g)),
-                                                     qf[k], sacc, 0, 0, 0);
+    for (int k = 0; k < kKsteps; ++k) sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[k], qf[k], sacc, 0, 0, 0);
     // sacc[v] = score of slot l32 with tile key 8 (v/4) + 4 g + v%4
     if (need_mask) {
       const int lim_g = lim - 4 * g;
@@ -1085,60 +1153,138 @@ __global__ __launch_bounds__(64) void attn_sq_group(focus_attn_desc d, float sc,
       bf16x8 pb;
 #pragma unroll
       for (int v = 0; v < 8; ++v) pb[v] = (__bf16)sacc[8 * m + v];
-      // keys of B slot v: 16 m + 8 (v/4) + 4 g + v%4
-      const int kb = 16 * m + 4 * (grp >> 1) + ri;
 #pragma unroll
-      for (int dt = 0; dt < kDtiles; ++dt) {
-        const int col_byte = 2 * (32 * dt + 16 * (grp & 1) + 4 * bq);
-        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vt + v_off<D>(kb, col_byte)));
-        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vt + v_off<D>(kb + 8, col_byte)));
-        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7),
-                                                           pb, oacc[dt], 0, 0, 0);
+      for (int dt = 0; dt < kDtiles; ++dt)
+        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[m * kDtiles + dt], pb, oacc[dt], 0, 0, 0);
+    }
+  };
+  // over this wave's lanes with a real summary (hi_l != kAll): min and max of hi_l
+  auto wave_range = [&](int hi_l, int& hi_min, int& hi_max) __attribute__((always_inline)) {
+    int a = hi_l, b = hi_l == kAll ? -1 : hi_l;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      a = min(a, __shfl_xor(a, o));
+      b = max(b, __shfl_xor(b, o));
+    }
+    hi_min = __builtin_amdgcn_readfirstlane(a);
+    hi_max = __builtin_amdgcn_readfirstlane(b);
+  };
+  // the two 32-row tiles of a 64-row cache stage (K at kst, V at vst)
+  auto stage_compute = [&](const char* kst, const char* vst, int row0, int hi_l, int hi_min, int hi_max)
+      __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int r0 = row0 + j * kBK;
+      if (hi_max >= r0) {
+        read_ops(kst + j * kTile, vst + j * kTile);
+        compute(hi_l - r0, r0 + kBK - 1 > hi_min);
       }
     }
   };
-  // A phase: nrows rows at (kbase, vbase); this lane sees rows <= hi_l;
-  // tiles past every lane's hi are skipped.  Two stages, the barrier closing
-  // each step also waits for the next tile's copies.
-  auto phase = [&](const char* kbase, const char* vbase, int nrows, int hi_l) __attribute__((always_inline)) {
-    int hi_min = hi_l, hi_max = hi_l;
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-      hi_min = min(hi_min, __shfl_xor(hi_min, o));
-      hi_max = max(hi_max, __shfl_xor(hi_max, o));
-    }
-    const int ntl = (min(nrows, hi_max + 1) + kBK - 1) / kBK;
-    if (ntl <= 0) return;
-    issue(kbase, vbase, 0, nrows, kbuf0, vbuf0);
-    __syncthreads();
-    for (int t = 0; t < ntl; t += 2) {
-      if (t + 1 < ntl) issue(kbase, vbase, (t + 1) * kBK, nrows, kbuf1, vbuf1);
-      compute(kbuf0, vbuf0, hi_l - t * kBK, t * kBK + kBK - 1 > hi_min);
-      __syncthreads();
-      if (t + 1 >= ntl) break;
-      if (t + 2 < ntl) issue(kbase, vbase, (t + 2) * kBK, nrows, kbuf0, vbuf0);
-      compute(kbuf1, vbuf1, hi_l - (t + 1) * kBK, (t + 1) * kBK + kBK - 1 > hi_min);
-      __syncthreads();
-    }
-  };
+  constexpr int kVm0 = (7 << 4) | (15 << 8);  // s_waitcnt vmcnt(0)
 
+  char* myreg = wave == 0 ? rg0 : wave == 1 ? rg1 : wave == 2 ? rg2 : rg3;
+  if constexpr (W == 8)
+    if (wave >= 4) myreg = wave == 4 ? rg4 : wave == 5 ? rg5 : wave == 6 ? rg6 : rg7;
   const char* kwin_all = reinterpret_cast<const char*>(reinterpret_cast<const __bf16*>(d.k) + (int64_t)hk * D);
   const char* vwin_all = reinterpret_cast<const char*>(reinterpret_cast<const __bf16*>(d.v) + (int64_t)hk * D);
   for (int k0 = 0; k0 < nk;) {
     // run [k0, k1) of windows on sequence b
-    const int b = wg_b[k0];
+    // (values read from LDS are the same in every lane: readfirstlane keeps
+    // them, and the addresses built from them, in scalar registers)
+    const int b = __builtin_amdgcn_readfirstlane(wg_b[k0]);
     int k1 = k0 + 1, cmax = wg_C[k0];
     while (k1 < nk && wg_b[k1] == b) cmax = max(cmax, wg_C[k1++]);
+    k1 = __builtin_amdgcn_readfirstlane(k1);
+    cmax = __builtin_amdgcn_readfirstlane(cmax);
+    // ---- cache phase, shared by the W waves
+    __syncthreads();  // every wave is past its window phase: regions 0-3 may be refilled
     if (cmax > 0) {
       const char* kc = reinterpret_cast<const char*>(reinterpret_cast<const __bf16*>(d.cache_k) +
                                                      ((int64_t)b * d.cache_cap * Hkv + hk) * D);
       const char* vc = reinterpret_cast<const char*>(reinterpret_cast<const __bf16*>(d.cache_v) +
                                                      ((int64_t)b * d.cache_cap * Hkv + hk) * D);
-      phase(kc, vc, cmax, kl < 0 ? kAll : (kl >= k0 && kl < k1) ? Cl - 1 : -1);
+      const int hi_l = kl < 0 ? kAll : (kl >= k0 && kl < k1) ? Cl - 1 : -1;
+      int hi_min, hi_max;
+      wave_range(hi_l, hi_min, hi_max);
+      const int nst = (cmax + 2 * kBK - 1) / (2 * kBK);
+      for (int i = wave; i < kStageCopies; i += W) copy_one(kc, vc, 0, cmax, rg0, rg1, i);
+      __builtin_amdgcn_s_waitcnt(kVm0);
+      __syncthreads();
+      for (int t = 0; t < nst; t += 2) {
+        if (t + 1 < nst)
+          for (int i = wave; i < kStageCopies; i += W) copy_one(kc, vc, (t + 1) * 2 * kBK, cmax, rg2, rg3, i);
+        stage_compute(rg0, rg1, t * 2 * kBK, hi_l, hi_min, hi_max);
+        __builtin_amdgcn_s_waitcnt(kVm0);
+        __syncthreads();
+        if (t + 1 >= nst) break;
+        if (t + 2 < nst)
+          for (int i = wave; i < kStageCopies; i += W) copy_one(kc, vc, (t + 2) * 2 * kBK, cmax, rg0, rg1, i);
+        stage_compute(rg2, rg3, (t + 1) * 2 * kBK, hi_l, hi_min, hi_max);
+        __builtin_amdgcn_s_waitcnt(kVm0);
+        __syncthreads();
+      }
     }
-    for (int k = k0; k < k1; ++k) {
-      const int64_t tok0 = wg_tok0[k];
-      phase(kwin_all + tok0 * row_bytes, vwin_all + tok0 * row_bytes, wg_nwk[k], kl < 0 ? kAll : kl == k ? pos : -1);
+    // the last barrier above also ends every read of the stages: the regions
+    // belong to their waves again
+    // ---- window phase: this wave's windows of the run, on its own, as one
+    // stream of 32-row tiles (the next window's first tile is copied while
+    // the current window's last tile is computed)
+    {
+      const int kend = min(k1, kw_hi + 1);
+      struct Win {
+        int k, ntl, hi_l, hi_min;
+        const char* kw;
+        const char* vw;
+        int nrows;
+      };
+      // the first window from k on that has rows for this wave's slots
+      auto find = [&](int k, Win& x) __attribute__((always_inline)) {
+        x.k = kend;
+        for (; k < kend; ++k) {
+          const int nrows = __builtin_amdgcn_readfirstlane(wg_nwk[k]);
+          const int hi_l = kl < 0 ? kAll : kl == k ? pos : -1;
+          int hi_min, hi_max;
+          wave_range(hi_l, hi_min, hi_max);
+          if (hi_max < 0 || nrows <= 0) continue;
+          const int64_t tok0 = wg_tok0[k];
+          const int64_t tok0_s =
+              (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(tok0 >> 32)) << 32) |
+                        (uint32_t)__builtin_amdgcn_readfirstlane((int)tok0));
+          x.k = k;
+          x.ntl = (min(nrows, hi_max + 1) + kBK - 1) / kBK;
+          x.hi_l = hi_l;
+          x.hi_min = hi_min;
+          x.kw = kwin_all + tok0_s * row_bytes;
+          x.vw = vwin_all + tok0_s * row_bytes;
+          x.nrows = nrows;
+          return;
+        }
+      };
+      auto issue_tile = [&](const Win& x, int t) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < kTileCopies; ++i) copy_one(x.kw, x.vw, t * kBK, x.nrows, myreg, myreg + kTile, i);
+      };
+      Win cur;
+      find(max(k0, kw_lo), cur);
+      if (cur.k < kend) issue_tile(cur, 0);
+      while (cur.k < kend) {
+        Win nxt;
+        nxt.k = kend;
+        for (int t = 0; t < cur.ntl; ++t) {
+          __builtin_amdgcn_s_waitcnt(kVm0);  // tile t has landed
+          read_ops(myreg, myreg + kTile);
+          __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): its operands are in registers
+          if (t + 1 < cur.ntl) {
+            issue_tile(cur, t + 1);
+          } else {
+            find(cur.k + 1, nxt);
+            if (nxt.k < kend) issue_tile(nxt, 0);
+          }
+          compute(cur.hi_l - t * kBK, t * kBK + kBK - 1 > cur.hi_min);
+        }
+        cur = nxt;
+      }
     }
     k0 = k1;
   }
@@ -1449,7 +1595,8 @@ extern "C" focus_status focus_window_attn(const focus_attn_desc* d, focus_stream
 
 // FOCUS adapter attention (Appendix A eq. focus-attn): the summary tokens of
 // every listed window attend over [cache ; window] under C(t) or the
-// k-mer-local rule; one wave of 32 summary slots per (window, head).
+// k-mer-local rule (C(t): many windows per workgroup; k-mer-local: one wave
+// of 32 summary slots per (window, head)).
 extern "C" focus_status focus_adapter_attn(const focus_adapter_desc* a, focus_stream_t stream) {
   if (!a) return FOCUS_E_NULL;
   if (a->dtype != FOCUS_BF16) return a->dtype == FOCUS_F32 ? FOCUS_E_UNSUPPORTED : FOCUS_E_DTYPE;
@@ -1505,17 +1652,21 @@ extern "C" focus_status focus_adapter_attn(const focus_adapter_desc* a, focus_st
   const float sc = scale * kLog2e;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const bool kl = a->mask == FOCUS_MASK_KMER_LOCAL;
-  if (!kl && t.max_window_summaries <= 32) {
-    // C(t): G windows per wave
-    const int G = (int)(32 / t.max_window_summaries);
+  constexpr int kSqWaves = 8;
+  if (!kl && t.max_window_summaries <= 32 * kSqWaves) {
+    // C(t): G windows per workgroup of kSqWaves waves; whole windows per wave
+    // while a window fits one wave's 32 slots
+    const int wpw = t.max_window_summaries <= 32 ? (int)(32 / t.max_window_summaries) : 0;
+    const int G = wpw > 0 ? kSqWaves * wpw : (int)(32 * kSqWaves / t.max_window_summaries);
     const int64_t n_groups = focus::ceil_div(nwl, G);
     const int64_t n_pairs_g = n_groups * a->n_heads;
     const int64_t blocks_g = focus::ceil_div(n_pairs_g, focus::kXcds) * focus::kXcds;
-    if (blocks_g * 64 >= ((int64_t)1 << 32)) return FOCUS_E_SHAPE;
+    if (blocks_g * 64 * kSqWaves >= ((int64_t)1 << 32)) return FOCUS_E_SHAPE;
+    const dim3 grid((uint32_t)blocks_g), block(64 * kSqWaves);
     if (a->head_dim == 128)
-      hipLaunchKernelGGL((attn_sq_group<128>), dim3((uint32_t)blocks_g), dim3(64), 0, s, d, sc, n_pairs_g, nwl, G, sq);
+      hipLaunchKernelGGL((attn_sq_block<128, kSqWaves>), grid, block, 0, s, d, sc, n_pairs_g, nwl, G, wpw, sq);
     else
-      hipLaunchKernelGGL((attn_sq_group<64>), dim3((uint32_t)blocks_g), dim3(64), 0, s, d, sc, n_pairs_g, nwl, G, sq);
+      hipLaunchKernelGGL((attn_sq_block<64, kSqWaves>), grid, block, 0, s, d, sc, n_pairs_g, nwl, G, wpw, sq);
     return focus::launch_status();
   }
   const int64_t n_pairs = nwl * a->n_heads;

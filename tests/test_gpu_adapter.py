@@ -35,6 +35,9 @@ CASES = [
     ([777, 1500], 1000, 0, 2, 2, 64),   # no summaries at all
     ([4096], 1024, 100, 8, 2, 64),
     ([130, 129, 64], 1000, 1, 2, 2, 128),
+    ([20000], 100, 10, 2, 2, 128),      # 200 windows: 25 per workgroup, windows across waves
+    ([3000, 1500, 2200], 100, 25, 2, 1, 64),  # 64 windows per workgroup, spanning sequences
+    ([600], 1000, 2, 2, 2, 128),        # 300 summaries per window: one workgroup per window
 ]
 
 
@@ -59,6 +62,34 @@ def test_adapter_attention_all_summaries(case, mask):
     o_ref, lse_ref = AD.adapter_attention(ref, to64(qs), to64(p.k), to64(p.v), mask)
     assert_parity(to64(o), o_ref, "bf16", f"adapter case {case} {mask}", lse.cpu().numpy().astype(np.float64),
                   lse_ref)
+
+
+@pytest.mark.parametrize("mask", list(MASKS))
+def test_adapter_attention_listed_windows(mask):
+    """A shuffled subset of the windows of a 200-window sequence and of a
+    second sequence (win_ids): only those windows' summaries are written, each
+    against its own cache prefix; the other rows keep what was there."""
+    seq, W, kmer, H, Hkv, D = [12000, 8000], 100, 10, 2, 2, 128
+    km = _kmer_for(seq, W, kmer, 0)
+    announce(f"adapter attn listed windows mask={mask}")
+    p = Prefill(seq, W, km, H, Hkv, D, "bf16", seed=3100, run=False)
+    ref = build_layout(seq, W, km)
+    rng = np.random.default_rng(3101)
+    wins = rng.permutation(ref["n_windows"])[:77].astype(np.int32)
+    qs = _sum_rows(p)
+    o = torch.full_like(qs, 7.0)
+    lse = torch.full((qs.shape[0], H), 7.0, dtype=torch.float32, device=DEV)
+    F.focus_adapter_attn(p.lay, qs, p.k, p.v, p.ck, p.cv, o_sum=o, lse_sum=lse, mask=MASKS[mask],
+                         win_ids=torch.as_tensor(wins, device=DEV), err=p.err)
+    torch.cuda.synchronize()
+    assert int(p.err.item()) == 0
+    listed = np.zeros(ref["n_summaries"], dtype=bool)
+    for x in wins:
+        listed[ref["win_sum_off"][x]:ref["win_sum_off"][x] + ref["win_nsum"][x]] = True
+    o_ref, lse_ref = AD.adapter_attention(ref, to64(qs), to64(p.k), to64(p.v), mask, windows=wins)
+    got, got_lse = to64(o), lse.cpu().numpy().astype(np.float64)
+    assert_parity(got[listed], o_ref[listed], "bf16", f"adapter listed {mask}", got_lse[listed], lse_ref[listed])
+    assert np.all(got[~listed] == 7.0) and np.all(got_lse[~listed] == 7.0)
 
 
 @pytest.mark.parametrize("mask", list(MASKS))
