@@ -41,6 +41,15 @@ sys.path.insert(0, ROOT)
 METRIC = "window-attention tokens/s at 1 Mb context; % MFMA peak (prefill), % HBM BW (decode)"
 PEAK_BF16_FLOPS = 2.5e15      # MI355X dense bf16 MFMA
 PEAK_HBM = 8.0e12             # MI355X HBM3E bytes/s
+# fp32 VALU issue without packed math: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
+# lane-instructions/s (a wave64 instruction takes 4 cycles of a SIMD; exp2,
+# log2 and sqrt take 8, measured, so they count as two)
+PEAK_VALU = 256 * 4 * 16 * 2.4e9
+# VALU work per (p, q) element pair of the fidelity metrics from logits, in
+# those units: per side max, shift-scale, exp2 (2), sum = 5; square roots of
+# the probabilities and the probabilities = 4; L1 2, L2 1, Hellinger 2; log2 p
+# and log2 q 2; KL 2; JS: exp2 (2), fma, log2 (2), max, add, sum, 2 fma = 10
+FID_VALU_PER_PAIR = 2 * 5 + 4 + 2 + 1 + 2 + 2 + 2 + 10
 ATTN_SOURCES = ["paper_2511_14694_amd/csrc/window_attn.hip", "paper_2511_14694_amd/csrc/common.h"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_window_attn_prefill_1mb.json")
 
@@ -569,7 +578,9 @@ def secondary_kmer_local(torch, F, fw, s, timer, reps=5):
 def secondary_fidelity(torch, F, fw, reps=5):
     """Fidelity metrics (L1, L2, Hellinger, JS, KL per position) over 1 M
     positions, for 4 nucleotides (f32 logits) and a 512-entry vocabulary (bf16
-    logits).  Bound by HBM: both logit rows are read once, 5 floats written."""
+    logits).  Both logit rows are read once and 5 floats written (HBM bound);
+    the per-element arithmetic (FID_VALU_PER_PAIR at PEAK_VALU) is the other
+    bound, and the larger of the two is the one reported as "bound"."""
     res = {}
     for name, (n, vocab, dtype) in fw.FIDELITY.items():
         p, q = fw.fidelity_logits(n, vocab, dtype, seed=fw.BASE_SEED, device="cuda:0")
@@ -583,8 +594,13 @@ def secondary_fidelity(torch, F, fw, reps=5):
         torch.cuda.synchronize()
         ms = sum(a.elapsed_time(b) for a, b in e) / reps
         nbytes = 2 * n * vocab * p.element_size() + n * F.FOCUS_FID_N * 4
+        valu = n * vocab * FID_VALU_PER_PAIR
+        t_hbm, t_alu = nbytes / PEAK_HBM, valu / PEAK_VALU
+        bound = "alu" if t_alu > t_hbm else "hbm"
         res[name] = {"positions": n, "vocab": vocab, "dtype": dtype, "ms": ms, "bytes": nbytes,
-                     "GBps": nbytes / ms / 1e6, "bound": "hbm", "frac_hbm": nbytes / (ms * 1e-3) / PEAK_HBM}
+                     "GBps": nbytes / ms / 1e6, "frac_hbm": nbytes / (ms * 1e-3) / PEAK_HBM,
+                     "valu_lane_ops": valu, "frac_alu": valu / (ms * 1e-3) / PEAK_VALU,
+                     "bound": bound, "frac": max(t_hbm, t_alu) / (ms * 1e-3)}
         del p, q, out
     return res
 
@@ -637,18 +653,31 @@ def secondary_adapter(torch, F, fw, reps=3, d_model=4096):
     a1.record()
     torch.cuda.synchronize()
     attn_ms = a0.elapsed_time(a1) / reps
+    nsum = lay["win_nsum"].cpu().numpy()
     st = lay["sum_tok"].cpu().numpy()
-    win_of = np.repeat(np.arange(tot.n_windows), lay["win_nsum"].cpu().numpy())
+    win_of = np.repeat(np.arange(tot.n_windows), nsum)
     rows = st - lay["win_tok_off"].cpu().numpy()[win_of]
-    pairs = int((lay["win_cache_off"].cpu().numpy()[win_of].astype(np.int64) + rows + 1).sum())
+    cache_off = lay["win_cache_off"].cpu().numpy().astype(np.int64)
+    pairs = int((cache_off[win_of] + rows + 1).sum())
     attn_flops = 4 * D * H * pairs
+    # algorithmic bytes: every K/V row a summary sees, once -- a window's rows
+    # up to its last summary's, and each sequence's cache prefix up to its
+    # largest C_w -- plus the summary queries read, outputs and LSE written
+    last = np.cumsum(nsum) - 1
+    win_rows = int((rows[last[nsum > 0]] + 1).sum())
+    seq_of = lay["win_seq"].cpu().numpy()
+    cache_rows = sum(int(cache_off[seq_of == b].max(initial=0)) for b in range(w.batch))
+    attn_bytes = 2 * Hkv * D * 2 * (win_rows + cache_rows) + 2 * ns * H * D * 2 + ns * H * 4
     gemm_flops = 2 * nt * d_model * 2 * Hkv * D + 2 * ns * d_model * H * D * 2
     flops = attn_flops + gemm_flops
     return {"workload": f"prefill_1mb layout, d_model {d_model}, {H} x {D} heads, bf16, random weights",
             "ms": ms, "tflops": flops / ms / 1e9, "frac_mfma": flops / (ms * 1e-3) / PEAK_BF16_FLOPS,
-            "gemm_flops": gemm_flops, "attention": {"ms": attn_ms, "visible_pairs_per_head": pairs,
-                                                    "tflops": attn_flops / attn_ms / 1e9,
-                                                    "frac_mfma": attn_flops / (attn_ms * 1e-3) / PEAK_BF16_FLOPS}}
+            "gemm_flops": gemm_flops,
+            "attention": {"ms": attn_ms, "visible_pairs_per_head": pairs, "bound": "hbm",
+                          "algorithmic_bytes": attn_bytes, "gb_per_s": attn_bytes / attn_ms / 1e6,
+                          "frac_hbm": attn_bytes / (attn_ms * 1e-3) / PEAK_HBM,
+                          "tflops": attn_flops / attn_ms / 1e9,
+                          "frac_mfma": attn_flops / (attn_ms * 1e-3) / PEAK_BF16_FLOPS}}
 
 
 def secondary_qkv_projection(torch, F, fw, reps=3, d_model=4096):

@@ -24,7 +24,6 @@ from __future__ import annotations
 import numpy as np
 
 from .adapter import round_bf16
-from .attention import compact
 
 
 def rope(x, pos, theta):
@@ -60,8 +59,3 @@ def qkv_project(layout, hidden, w_qkv, n_heads, n_kv_heads, theta=10000.0, store
     if store_bf16:
         q, k, v = round_bf16(q), round_bf16(k), round_bf16(v)
     return q, k, v
-
-
-def cache_of(layout, k_all, v_all, b):
-    """The retained cache of sequence b from K, V of every token."""
-    return compact(layout, k_all, v_all, b)

@@ -251,6 +251,163 @@ __global__ __launch_bounds__(kThreads) void fid_rows_wave(focus_fidelity_desc d)
   if (lane == 0) m.store(d.out + t * FOCUS_FID_N);
 }
 
+// Sums / extrema over the 32 lanes of a half-wave, the result in each of them.
+__device__ inline float half_sum(float x) {
+  x = focus::sum8(x);
+  x += dpp_mirror16(x);
+  return x + __shfl_xor(x, 16);
+}
+__device__ inline float half_max(float x) {
+  x = fmaxf(x, focus::dpp_xor1(x));
+  x = fmaxf(x, focus::dpp_xor2(x));
+  x = fmaxf(x, focus::dpp_half_mirror(x));
+  x = fmaxf(x, dpp_mirror16(x));
+  return fmaxf(x, __shfl_xor(x, 16));
+}
+__device__ inline float half_min(float x) { return -half_max(-x); }
+
+// Logits rows with 64 < vocab <= 32 NPL read 16 bytes per lane per load: half
+// a wave (32 lanes) per position, two positions per wave.
+//
+// Fewer operations per element than fid_rows_wave:
+// * e = 2^((x - max) log2(e) / 2) is the square root of the unnormalised
+//   probability: p = e^2 rp (rp = 1 / sum e^2) and sqrt(p) = e sqrt(rp), so
+//   one exponential per element gives both, and the Hellinger term needs no
+//   square root;
+// * when the smallest probability of both rows is at least twice the clip
+//   (decided from the row minimum of the logits), the clip changes nothing and
+//   the renormalised sum is 1: that pass is skipped.  Otherwise the clip and
+//   the renormalisation are applied as in fid_rows_wave;
+// * log2 p and log2 q come from the logits, and the mixture's logarithm from
+//   r = log2 q - log2 p: log2 m - log2 p = max(r, 0) + log2((1 + 2^-|r|) / 2),
+//   so the JS term is q r - (p + q) that (exactly zero when p = q).
+template <typename T, int NPL, bool FULL>
+__global__ __launch_bounds__(kThreads) void fid_logits_half(focus_fidelity_desc d) {
+  // every fused multiply-add below is written out: a product contracted into
+  // one side of p - q but not the other would break the exact zero of p = q
+#pragma clang fp contract(off)
+  constexpr int kVec = 16 / sizeof(T);
+  static_assert(NPL % kVec == 0, "whole 16-byte loads per lane");
+  constexpr float kH = 0.5f * kLog2e;
+  const int lane = threadIdx.x & 31;
+  const int64_t t = (int64_t)blockIdx.x * (kThreads / 32) + (threadIdx.x >> 5);
+  if (t >= d.n_pos) return;  // a whole half-wave: the cross-lane steps stay inside a half
+  const int V = d.vocab;
+  const T* pr = reinterpret_cast<const T*>(d.p) + t * V;
+  const T* qr = reinterpret_cast<const T*>(d.q) + t * V;
+  bool ok[NPL];
+  float xp[NPL], xq[NPL];
+#pragma unroll
+  for (int c = 0; c < NPL / kVec; ++c) {
+    const int i0 = c * 32 * kVec + lane * kVec;
+    uint4 wp = make_uint4(0, 0, 0, 0), wq = wp;
+    if (FULL || i0 < V) {
+      wp = *reinterpret_cast<const uint4*>(pr + i0);
+      wq = *reinterpret_cast<const uint4*>(qr + i0);
+    }
+    const T* ep = reinterpret_cast<const T*>(&wp);
+    const T* eq = reinterpret_cast<const T*>(&wq);
+#pragma unroll
+    for (int j = 0; j < kVec; ++j) {
+      ok[c * kVec + j] = FULL || i0 < V;
+      xp[c * kVec + j] = (float)ep[j];
+      xq[c * kVec + j] = (float)eq[j];
+    }
+  }
+  float mp = -INFINITY, mq = -INFINITY, np_ = INFINITY, nq = INFINITY;
+#pragma unroll
+  for (int k = 0; k < NPL; ++k)
+    if (ok[k]) {
+      mp = fmaxf(mp, xp[k]);
+      mq = fmaxf(mq, xq[k]);
+      np_ = fminf(np_, xp[k]);
+      nq = fminf(nq, xq[k]);
+    }
+  mp = half_max(mp);
+  mq = half_max(mq);
+  np_ = half_min(np_);
+  nq = half_min(nq);
+  const float mph = mp * kH, mqh = mq * kH;
+  // y = log2 of the unnormalised probability, halved; e = 2^y
+  float yp[NPL], yq[NPL], ep[NPL], eq[NPL];
+  float sp = 0.f, sq = 0.f;
+#pragma unroll
+  for (int k = 0; k < NPL; ++k) {
+    yp[k] = fmaf(xp[k], kH, -mph);
+    yq[k] = fmaf(xq[k], kH, -mqh);
+    ep[k] = __builtin_amdgcn_exp2f(yp[k]);
+    eq[k] = __builtin_amdgcn_exp2f(yq[k]);
+    if (ok[k]) {
+      sp = fmaf(ep[k], ep[k], sp);
+      sq = fmaf(eq[k], eq[k], sq);
+    }
+  }
+  sp = half_sum(sp);
+  sq = half_sum(sq);
+  const float rp = 1.f / sp, rq = 1.f / sq;
+  const float lsp = __builtin_amdgcn_logf(sp), lsq = __builtin_amdgcn_logf(sq);
+  const float emp = __builtin_amdgcn_exp2f(fmaf(np_, kH, -mph)), emq = __builtin_amdgcn_exp2f(fmaf(nq, kH, -mqh));
+  const bool fast = emp * emp * rp >= 2.f * kClip && emq * emq * rq >= 2.f * kClip;
+
+  float l1 = 0.f, l2 = 0.f, h = 0.f, js = 0.f, kl = 0.f;
+  // one pair: probabilities pn, qn, their square roots a, b and base-2 logs lp, lq
+  auto add = [&](float pn, float qn, float a, float b, float lp, float lq) __attribute__((always_inline)) {
+    const float dd = pn - qn;
+    l1 += fabsf(dd);
+    l2 = fmaf(dd, dd, l2);
+    const float sd = a - b;
+    h = fmaf(sd, sd, h);
+    const float r = lq - lp;
+    kl = fmaf(pn, -r, kl);
+    const float g = fmaxf(r, 0.f) + __builtin_amdgcn_logf(fmaf(0.5f, __builtin_amdgcn_exp2f(-fabsf(r)), 0.5f));
+    js = fmaf(qn, r, js);
+    js = fmaf(-(pn + qn), g, js);
+  };
+  if (fast) {
+    const float srp = __builtin_amdgcn_sqrtf(rp), srq = __builtin_amdgcn_sqrtf(rq);
+#pragma unroll
+    for (int k = 0; k < NPL; ++k) {
+      if (!ok[k]) continue;
+      const float a = ep[k] * srp, b = eq[k] * srq;
+      add(a * a, b * b, a, b, fmaf(yp[k], 2.f, -lsp), fmaf(yq[k], 2.f, -lsq));
+    }
+  } else {
+    // the clip at 1e-12 and the renormalisation, as in fid_rows_wave
+    float p[NPL], q[NPL];
+    float cp = 0.f, cq = 0.f;
+#pragma unroll
+    for (int k = 0; k < NPL; ++k) {
+      p[k] = fmaxf(ep[k] * ep[k] * rp, kClip);
+      q[k] = fmaxf(eq[k] * eq[k] * rq, kClip);
+      if (ok[k]) {
+        cp += p[k];
+        cq += q[k];
+      }
+    }
+    cp = half_sum(cp);
+    cq = half_sum(cq);
+    const float rcp = 1.f / cp, rcq = 1.f / cq;
+    const float lcp = __builtin_amdgcn_logf(cp), lcq = __builtin_amdgcn_logf(cq);
+    const float lclip = __builtin_amdgcn_logf(kClip);
+#pragma unroll
+    for (int k = 0; k < NPL; ++k) {
+      if (!ok[k]) continue;
+      const float pn = p[k] * rcp, qn = q[k] * rcq;
+      const float lp = (p[k] > kClip ? fmaf(yp[k], 2.f, -lsp) : lclip) - lcp;
+      const float lq = (q[k] > kClip ? fmaf(yq[k], 2.f, -lsq) : lclip) - lcq;
+      // pn, qn >= 1e-12 / 1.x: no denormals for the bare v_sqrt_f32
+      add(pn, qn, __builtin_amdgcn_sqrtf(pn), __builtin_amdgcn_sqrtf(qn), lp, lq);
+    }
+  }
+  Sums m;
+  m.l1 = half_sum(l1);
+  m.l2 = half_sum(l2);
+  m.h = half_sum(h);
+  m.js = half_sum(js);
+  m.kl = half_sum(kl);
+  if (lane == 0) m.store(d.out + t * FOCUS_FID_N);
+}
+
 // Mean of each metric over a sequence's positions: one workgroup per
 // sequence, a fixed-order tree sum (deterministic).
 __global__ __launch_bounds__(kThreads) void fid_seq_mean(focus_fidelity_desc d) {
@@ -316,14 +473,25 @@ extern "C" focus_status focus_fidelity(const focus_fidelity_desc* d, focus_strea
     else if (vec) hipLaunchKernelGGL((fid_rows_wave<T, true, 8, false>), grid, block, 0, s, *d);   \
     else hipLaunchKernelGGL((fid_rows_wave<T, false, 8, false>), grid, block, 0, s, *d);           \
   }
+    // logits rows of 64 < vocab <= 512 with 16-byte loads: two positions per wave
+    const bool half = vec && d->input_kind == FOCUS_FID_LOGITS && d->vocab > 64 && d->vocab <= 512;
+    const dim3 grid_h((uint32_t)focus::ceil_div(d->n_pos, kThreads / 32));
+#define FOCUS_FID_HALF(T)                                                                                  \
+  if (d->vocab == 512) hipLaunchKernelGGL((fid_logits_half<T, 16, true>), grid_h, block, 0, s, *d);         \
+  else if (d->vocab > 256) hipLaunchKernelGGL((fid_logits_half<T, 16, false>), grid_h, block, 0, s, *d);    \
+  else if (d->vocab == 256) hipLaunchKernelGGL((fid_logits_half<T, 8, true>), grid_h, block, 0, s, *d);     \
+  else hipLaunchKernelGGL((fid_logits_half<T, 8, false>), grid_h, block, 0, s, *d);
     if (d->dtype == FOCUS_BF16) {
       if (small) hipLaunchKernelGGL(fid_rows_small<__bf16>, grid, block, 0, s, *d);
+      else if (half) { FOCUS_FID_HALF(__bf16) }
       else { FOCUS_FID_WAVE(__bf16) }
     } else {
       if (small) hipLaunchKernelGGL(fid_rows_small<float>, grid, block, 0, s, *d);
+      else if (half) { FOCUS_FID_HALF(float) }
       else { FOCUS_FID_WAVE(float) }
     }
 #undef FOCUS_FID_WAVE
+#undef FOCUS_FID_HALF
     focus_status st = focus::launch_status();
     if (st != FOCUS_OK) return st;
   }
