@@ -78,26 +78,50 @@ struct Item {
 };
 
 // Block -> (listed window, head, query tile).  Blocks go round robin over the
-// XCDs, and the QT query tiles of a (window, head) pair get consecutive blocks
-// of one XCD (they share its K/V tiles through that XCD's L2).  When H is a
-// multiple of the XCD count, XCD x owns heads x, x + 8, ... and walks them one
-// at a time, each over all listed windows in list order: the workgroups that
-// run together on an XCD then stream the same cache rows of one head at about
-// the same time, so each row is fetched into its L2 once for all of them.
-// Otherwise pair p = list_idx * H + h goes to XCD p % 8, in increasing p.
-// A pair's query tiles go last-first: under the causal window mask the last
-// tile sees the most keys, and starting the longest workgroups first shortens
-// the tail of a launch (a 32 000-token dense window: 8.6 -> 7.7 ms).
+// XCDs.  When H is a multiple of the XCD count, XCD x owns heads x, x + 8, ...
+// and walks them one at a time, each over all listed windows in list order:
+// the workgroups that run together on an XCD then stream the same cache rows
+// of one head at about the same time, so each row is fetched into its L2 once
+// for all of them.  Otherwise pair p = list_idx * H + h goes to XCD p % 8, in
+// increasing p.  The QT query tiles of a pair go last-first (under the causal
+// window mask the last tile sees the most keys, and starting the longest
+// workgroups first shortens the tail of a launch).
+//
+// Two orders of an XCD's blocks (H a multiple of 8):
+// * ROUNDS = false: a pair's query tiles are consecutive blocks (they share
+//   the window's K/V through the XCD's L2 while they run together);
+// * ROUNDS = true: kRound consecutive blocks (one per compute unit of the XCD)
+//   are one query tile of kRound pairs, the next kRound the next query tile of
+//   the same pairs.  The hardware hands an XCD's blocks to its compute units in
+//   a fixed rotation, so with the first order each compute unit always gets
+//   the same query tile, and the ones with short tiles wait every round for
+//   the ones with long tiles (per-workgroup timestamps: ~12 us idle per
+//   workgroup at 1 Mb).  With one tile per round the workgroups of a round
+//   last about equally long.  It pays where the arithmetic dominates (the C(t)
+//   attention: 1 Mb 88.6 -> 86.7 ms, 100 kb 2.70 -> 2.58 ms); the HBM-bound
+//   k-mer-local launch loses more from the scattered K/V reuse (9.6 -> 10.5 ms)
+//   and keeps the first order.
+constexpr int64_t kRound = 32;  // compute units per XCD on MI355X (256 / 8)
+template <bool ROUNDS = false>
 __device__ inline Item map_block(int64_t bid, int64_t n_pairs, int H, int QT) {
   const int x = (int)(bid % focus::kXcds);
   const int64_t s = bid / focus::kXcds;
   Item it;
   it.qt = QT - 1 - (int)(s % QT);
-  const int64_t j = s / QT;  // this XCD's j-th pair
+  int64_t j = s / QT;  // this XCD's j-th pair
   if (H % focus::kXcds == 0) {
+    bool in_range = true;
+    if (ROUNDS) {
+      const int64_t npx = n_pairs / focus::kXcds;  // pairs of this XCD
+      const int64_t c = s / (kRound * QT), r = s % (kRound * QT);
+      const int64_t m = min(kRound, npx - c * kRound);  // pairs in this group of rounds
+      in_range = m > 0 && r < m * QT;
+      j = c * kRound + (in_range ? r % m : 0);
+      it.qt = QT - 1 - (in_range ? (int)(r / m) : 0);
+    }
     const int64_t nwl = n_pairs / H;  // listed windows
     const int64_t hl = nwl > 0 ? j / nwl : 0;
-    it.valid = nwl > 0 && hl < H / focus::kXcds;
+    it.valid = in_range && nwl > 0 && hl < H / focus::kXcds;
     it.list_idx = nwl > 0 ? j % nwl : 0;
     it.h = (int)(hl * focus::kXcds + x);
   } else {
@@ -548,7 +572,7 @@ __global__ __launch_bounds__(512, 2) void attn_ct(
     split = (int)(r % sp.n);
     bid = (r / sp.n) * focus::kXcds + bid % focus::kXcds;
   }
-  const Item it = map_block(bid, n_pairs, d.n_heads, QT);
+  const Item it = map_block<true>(bid, n_pairs, d.n_heads, QT);
   if (!it.valid) return;
   const int64_t gw = listed_window(d, it.list_idx);
   if (gw < 0 || gw >= d.totals.n_windows) {
