@@ -123,6 +123,67 @@ __global__ __launch_bounds__(kThreads) void fid_rows_small(focus_fidelity_desc d
   m.store(d.out + t * FOCUS_FID_N);
 }
 
+// Four categories (the nucleotides), rows 16-byte (float) or 8-byte (bf16)
+// aligned: one thread per position, each row in one load, and the softmax,
+// clip and renormalisation by reciprocals (one division per row instead of one
+// per element).  Contraction is off: a product fused into one side of p - q
+// but not the other would break the exact zero of identical rows.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void fid_rows4(focus_fidelity_desc d) {
+#pragma clang fp contract(off)
+  const int64_t t = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (t >= d.n_pos) return;
+  float p[4], q[4];
+  if constexpr (sizeof(T) == 4) {
+    const float4 a = reinterpret_cast<const float4*>(d.p)[t];
+    const float4 b = reinterpret_cast<const float4*>(d.q)[t];
+    p[0] = a.x, p[1] = a.y, p[2] = a.z, p[3] = a.w;
+    q[0] = b.x, q[1] = b.y, q[2] = b.z, q[3] = b.w;
+  } else {
+    const uint2 a = reinterpret_cast<const uint2*>(d.p)[t];
+    const uint2 b = reinterpret_cast<const uint2*>(d.q)[t];
+    const uint32_t wa[2] = {a.x, a.y}, wb[2] = {b.x, b.y};
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      p[2 * i] = __uint_as_float(wa[i] << 16);
+      p[2 * i + 1] = __uint_as_float(wa[i] & 0xFFFF0000u);
+      q[2 * i] = __uint_as_float(wb[i] << 16);
+      q[2 * i + 1] = __uint_as_float(wb[i] & 0xFFFF0000u);
+    }
+  }
+  if (d.input_kind == FOCUS_FID_LOGITS) {
+    const float mp = fmaxf(fmaxf(p[0], p[1]), fmaxf(p[2], p[3]));
+    const float mq = fmaxf(fmaxf(q[0], q[1]), fmaxf(q[2], q[3]));
+    float sp = 0.f, sq = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      p[i] = __builtin_amdgcn_exp2f((p[i] - mp) * kLog2e);
+      q[i] = __builtin_amdgcn_exp2f((q[i] - mq) * kLog2e);
+      sp += p[i];
+      sq += q[i];
+    }
+    const float rp = 1.f / sp, rq = 1.f / sq;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      p[i] *= rp;
+      q[i] *= rq;
+    }
+  }
+  float cp = 0.f, cq = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    p[i] = fmaxf(p[i], kClip);
+    q[i] = fmaxf(q[i], kClip);
+    cp += p[i];
+    cq += q[i];
+  }
+  const float rcp = 1.f / cp, rcq = 1.f / cq;
+  Sums m;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) m.add(p[i] * rcp, q[i] * rcq);
+  m.store(d.out + t * FOCUS_FID_N);
+}
+
 // One wave per position, kSmallV < vocab <= 64 * NPL (NPL = 8 or 16).  VEC: the row is
 // read 16 bytes per lane per load (kVec elements), else one element per load.
 // Logarithms of the clipped, renormalised probabilities come straight from the
@@ -481,12 +542,17 @@ extern "C" focus_status focus_fidelity(const focus_fidelity_desc* d, focus_strea
   else if (d->vocab > 256) hipLaunchKernelGGL((fid_logits_half<T, 16, false>), grid_h, block, 0, s, *d);    \
   else if (d->vocab == 256) hipLaunchKernelGGL((fid_logits_half<T, 8, true>), grid_h, block, 0, s, *d);     \
   else hipLaunchKernelGGL((fid_logits_half<T, 8, false>), grid_h, block, 0, s, *d);
+    // four categories, rows aligned for one load each
+    const bool rows4 = d->vocab == 4 && (reinterpret_cast<uintptr_t>(d->p) % (4 * eb)) == 0 &&
+                       (reinterpret_cast<uintptr_t>(d->q) % (4 * eb)) == 0;
     if (d->dtype == FOCUS_BF16) {
-      if (small) hipLaunchKernelGGL(fid_rows_small<__bf16>, grid, block, 0, s, *d);
+      if (rows4) hipLaunchKernelGGL(fid_rows4<__bf16>, grid, block, 0, s, *d);
+      else if (small) hipLaunchKernelGGL(fid_rows_small<__bf16>, grid, block, 0, s, *d);
       else if (half) { FOCUS_FID_HALF(__bf16) }
       else { FOCUS_FID_WAVE(__bf16) }
     } else {
-      if (small) hipLaunchKernelGGL(fid_rows_small<float>, grid, block, 0, s, *d);
+      if (rows4) hipLaunchKernelGGL(fid_rows4<float>, grid, block, 0, s, *d);
+      else if (small) hipLaunchKernelGGL(fid_rows_small<float>, grid, block, 0, s, *d);
       else if (half) { FOCUS_FID_HALF(float) }
       else { FOCUS_FID_WAVE(float) }
     }
