@@ -1,9 +1,9 @@
 """GPU parity of focus_fidelity against the float64 oracle.
 
-Every position of small cases (vocab 1 .. 1024 across the one-thread and
-one-wave paths, logits and probabilities with exact zeros, bf16 and f32,
-sequences including empty ones) and sampled positions of the two full-size
-workloads (1 M positions of 4 nucleotides, 1 M positions of a 512-entry
+Every position of small cases (vocab 1 .. 1024 across the one-thread,
+half-wave and one-wave paths, logits and probabilities with exact zeros,
+logits far enough below the rest that the clip acts, bf16 and f32, sequences
+including empty ones) and sampled positions of the two full-size workloads (1 M positions of 4 nucleotides, 1 M positions of a 512-entry
 vocabulary).  Tolerance (float32 arithmetic against float64 on the same
 inputs): |got - ref| <= 2e-5 + 2e-5 |ref| per metric; identical inputs give
 exact zeros.
@@ -51,6 +51,25 @@ def test_small_all_positions(vocab, dtype, kind):
     ref = FD.metrics_from_logits(pp, qq) if kind == "logits" else FD.metrics(pp, qq)
     _check(out.cpu().numpy().astype(np.float64), ref, f"per-position v{vocab}")
     _check(mean.cpu().numpy().astype(np.float64), FD.sequence_means(ref, cu), f"means v{vocab}")
+
+
+@pytest.mark.parametrize("vocab", [4, 100, 256, 512])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_logits_that_clip(vocab, dtype):
+    """Rows whose softmax puts some entries below the 1e-12 clip (logits 60
+    below the rest) next to rows that clip nothing: the clip-and-renormalise
+    path and the path that skips it, in one launch."""
+    announce(f"fidelity clipped logits v{vocab} {dtype}")
+    n = 513
+    p, q = fw.fidelity_logits(n, vocab, "f32", seed=vocab + 11, device=DEV)
+    p[::3, : max(1, vocab // 7)] -= 60.0       # every third row of p clips
+    q[1::4, -1] -= 60.0                        # every fourth row of q clips one entry
+    if dtype == "bf16":
+        p, q = p.to(torch.bfloat16), q.to(torch.bfloat16)
+    out, _ = F.focus_fidelity(p.contiguous(), q.contiguous())
+    torch.cuda.synchronize()
+    ref = FD.metrics_from_logits(to64(p), to64(q))
+    _check(out.cpu().numpy().astype(np.float64), ref, f"clipped logits v{vocab} {dtype}")
 
 
 @pytest.mark.parametrize("vocab", [4, 512])
