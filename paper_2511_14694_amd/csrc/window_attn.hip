@@ -139,11 +139,12 @@ __device__ inline int64_t listed_window(const focus_attn_desc& d, int64_t li) {
 
 // ------------------------------------------------------------------ bf16 MFMA
 
-template <int D, int W>
+template <int D, int W, int BK = 64>
 struct Cfg {
   static constexpr int kWaves = W;                        // 32 query rows per wave
   static constexpr int kBQ = 32 * W;                      // query rows per block
-  static constexpr int kBK = 64;                          // keys per tile
+  static constexpr int kBK = BK;                          // keys per tile
+  static constexpr int kSt = BK / 32;                     // 32-key MFMA blocks per tile
   static constexpr int kThreads = 64 * W;
   static constexpr int kRB = D * 2;                       // bytes per row
   static constexpr int kTile = kBK * kRB;                 // bytes per tile per tensor
@@ -199,16 +200,26 @@ constexpr Split kNoSplit = {1, nullptr, nullptr, 0, 0};
 
 // The k-mer-local and summary-query modes (the C(t) window attention is
 // attn_ct below).
+//
+// The k-mer-local window attention (KL, not SQ) visits only a handful of
+// tiles per workgroup (the summary list and the window rows of its k-mers),
+// so it is bound by the latency of each tile's copy: it takes 32-key tiles
+// through four LDS stages, three tiles in flight while one is computed (64 KB,
+// two workgroups per compute unit).  The summary-query mode keeps 64-key
+// tiles through two stages.
 template <int D, int W, bool KL, bool SQ>
 __global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_desc d, float sc, int64_t n_pairs,
                                                                      int QT, SumQ sq) {
   static_assert(KL || SQ, "C(t) window attention is attn_ct");
-  using C = Cfg<D, W>;
-  // Two K and two V tile buffers as separate arrays, referenced statically by
-  // a loop unrolled by two: the compiler can then tell a tile being read from
-  // the one being filled, and waits for the copies only at the barrier.
+  constexpr bool kDeep = KL && !SQ;
+  using C = Cfg<D, W, kDeep ? 32 : 64>;
+  // K and V tile buffers as separate arrays, referenced statically by a loop
+  // unrolled by the stage count: the compiler can then tell a tile being read
+  // from the ones being filled, and waits for the copies only where it must.
   __shared__ __attribute__((aligned(1024))) char kbuf0[C::kTile], kbuf1[C::kTile];
   __shared__ __attribute__((aligned(1024))) char vbuf0[C::kTile], vbuf1[C::kTile];
+  __shared__ __attribute__((aligned(1024))) char kbuf2[kDeep ? C::kTile : 16], kbuf3[kDeep ? C::kTile : 16];
+  __shared__ __attribute__((aligned(1024))) char vbuf2[kDeep ? C::kTile : 16], vbuf3[kDeep ? C::kTile : 16];
 
   const int tid = threadIdx.x;
   const Item it = map_block(blockIdx.x, n_pairs, d.n_heads, QT);
@@ -378,7 +389,7 @@ __global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_d
   const int grp = lane >> 4, ri = (lane >> 2) & 3, bq = lane & 3;
 
   auto compute_tile = [&](int t, const char* kl, const char* vl) {
-    // Key kk of the tile (0..63) is visible to this lane's query iff kk <= lim:
+    // Key kk of the tile (0 .. kBK - 1) is visible to this lane's query iff kk <= lim:
     // cache tiles hide only rows past Cw, window tiles are causal.
     const bool in_cache = t < nct;  // (k-mer-local: the summary list)
     const int row0 = in_cache ? t * C::kBK : (t - nct + tw0) * C::kBK;
@@ -388,11 +399,11 @@ __global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_d
     const int lim = KL ? (in_cache ? jq - row0 : qi - row0) : (in_cache ? Cw - row0 - 1 : qi - row0);
     const int lo = KL ? (in_cache ? (Cw > 0 ? 0 : 1) - row0 : qlo - row0) : 0;
     if (live) {
-      // S^T = K Q^T: the two 32-key blocks as two independent MFMA chains,
+      // S^T = K Q^T: the tile's 32-key blocks as independent MFMA chains,
       // each K operand read one k-step ahead of its MFMA.
-      f32x16 sacc[2];
+      f32x16 sacc[C::kSt];
 #pragma unroll
-      for (int st = 0; st < 2; ++st)
+      for (int st = 0; st < C::kSt; ++st)
 #pragma unroll
         for (int v = 0; v < 16; ++v) sacc[st][v] = 0.f;
       // Per-lane LDS offsets are rebuilt each step behind an empty asm
@@ -406,25 +417,25 @@ __global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_d
         asm volatile("" : "+v"(ko));
         return *reinterpret_cast<const bf16x8*>(kl + (ko + st * 32 * C::kRB));
       };
-      bf16x8 ka[2], kn[2];
+      bf16x8 ka[C::kSt], kn[C::kSt];
 #pragma unroll
-      for (int st = 0; st < 2; ++st) ka[st] = kread(0, st);
+      for (int st = 0; st < C::kSt; ++st) ka[st] = kread(0, st);
 #pragma unroll
       for (int s = 0; s < C::kKsteps; ++s) {
         if (s + 1 < C::kKsteps) {
 #pragma unroll
-          for (int st = 0; st < 2; ++st) kn[st] = kread(s + 1, st);
+          for (int st = 0; st < C::kSt; ++st) kn[st] = kread(s + 1, st);
         }
 #pragma unroll
-        for (int st = 0; st < 2; ++st) sacc[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[st], qf[s], sacc[st], 0, 0, 0);
+        for (int st = 0; st < C::kSt; ++st) sacc[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[st], qf[s], sacc[st], 0, 0, 0);
 #pragma unroll
-        for (int st = 0; st < 2; ++st) ka[st] = kn[st];
+        for (int st = 0; st < C::kSt; ++st) ka[st] = kn[st];
       }
       // sacc[st][v] = score of query qi with tile key 32 st + 8 (v/4) + 4 g + v%4
       if (need_mask) {
         const int lim_g = lim - 4 * g, lo_g = lo - 4 * g;
 #pragma unroll
-        for (int st = 0; st < 2; ++st)
+        for (int st = 0; st < C::kSt; ++st)
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
             const int kk = st * 32 + (v >> 2) * 8 + (v & 3);
@@ -433,7 +444,7 @@ __global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_d
       }
       float mx = -INFINITY;
 #pragma unroll
-      for (int st = 0; st < 2; ++st)
+      for (int st = 0; st < C::kSt; ++st)
 #pragma unroll
         for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[st][v]);
       {
@@ -452,7 +463,7 @@ __global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_d
       }
       float psum = 0.f;
 #pragma unroll
-      for (int st = 0; st < 2; ++st)
+      for (int st = 0; st < C::kSt; ++st)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const float p = __builtin_amdgcn_exp2f(fmaf(sacc[st][v], sc, -m_run));
@@ -461,7 +472,7 @@ __global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_d
         }
       l_run += psum;
 #pragma unroll
-      for (int st = 0; st < 2; ++st) {
+      for (int st = 0; st < C::kSt; ++st) {
 #pragma unroll
         for (int m = 0; m < 2; ++m) {
           bf16x8 pb;
@@ -487,7 +498,43 @@ __global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_d
     }
   };
 
-  {
+  if constexpr (kDeep) {
+    // Step u: copies of tile u + 3 into the stage tile u - 1 left, tile u
+    // computed, then this wave waits until its copies of tile u + 1 have
+    // landed (those of u + 2 and u + 3 may stay in flight) and the barrier
+    // makes that true for every wave's share.
+    constexpr int kPer = 2 * kDma;  // copies a wave issues per tile
+    auto wait_next = [&](int u) __attribute__((always_inline)) {
+      const int younger = max(0, min(2, ntiles - 2 - u));  // tiles u + 2, u + 3 issued
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
+      if (younger == 2)
+        __builtin_amdgcn_s_waitcnt(((2 * kPer) & 15) | (((2 * kPer) >> 4) << 14) | (7 << 4) | (15 << 8));
+      else if (younger == 1)
+        __builtin_amdgcn_s_waitcnt((kPer & 15) | ((kPer >> 4) << 14) | (7 << 4) | (15 << 8));
+      else
+        __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
+      __builtin_amdgcn_s_barrier();
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    };
+    auto step = [&](int u, const char* kc, const char* vc, char* kn, char* vn) __attribute__((always_inline)) {
+      if (u + 3 < ntiles) issue_tile(u + 3, kn, vn);
+      compute_tile(u, kc, vc);
+      wait_next(u);
+    };
+    issue_tile(0, kbuf0, vbuf0);
+    if (1 < ntiles) issue_tile(1, kbuf1, vbuf1);
+    if (2 < ntiles) issue_tile(2, kbuf2, vbuf2);
+    wait_next(-1);  // tile 0 has landed
+    for (int t = 0; t < ntiles; t += 4) {
+      step(t, kbuf0, vbuf0, kbuf3, vbuf3);
+      if (t + 1 >= ntiles) break;
+      step(t + 1, kbuf1, vbuf1, kbuf0, vbuf0);
+      if (t + 2 >= ntiles) break;
+      step(t + 2, kbuf2, vbuf2, kbuf1, vbuf1);
+      if (t + 3 >= ntiles) break;
+      step(t + 3, kbuf3, vbuf3, kbuf2, vbuf2);
+    }
+  } else {
     // The barrier closing each step also waits for the next tile's copies.
     issue_tile(0, kbuf0, vbuf0);
     __syncthreads();
