@@ -35,8 +35,9 @@
 // listed windows are started in list order (last window = largest cache first
 // by default).
 //
-// The k-mer-local mask (attn_bf16<D, 4, true, false>) keeps the simpler
-// two-stage form of the same MFMA scheme: 4 waves, each copying its share.
+// The k-mer-local mask (attn_bf16<D, 4, true, false>) uses the same MFMA
+// scheme without the software pipeline: 4 waves, each copying its share of
+// 32-key tiles through four LDS stages.
 //
 // Summary queries (the FOCUS adapter's attention): under C(t) several windows'
 // summaries share one workgroup (attn_sq_block); otherwise the bf16 kernel
