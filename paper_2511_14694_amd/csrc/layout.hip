@@ -9,7 +9,7 @@
 // Two launches:
 //   layout_windows  one workgroup; scans over sequences and windows (the number
 //                   of windows is small: 1 000 per megabase at W = 1 000)
-//   layout_tokens   one thread per augmented token; a closed form places the
+//   layout_tokens   four augmented tokens per thread; a closed form places a
 //                   token inside its window: with groups of k_w bases + 1
 //                   summary, token i of the window is in group i / (k_w + 1),
 //                   and it is that group's summary when its offset equals the
@@ -21,6 +21,7 @@ namespace {
 constexpr int kScanThreads = 1024;
 constexpr int kScanWaves = kScanThreads / 64;
 constexpr int kTokThreads = 256;
+constexpr int kTokPerThread = 4;
 
 // Exclusive scan of one int64 per thread across the workgroup; *total gets the
 // workgroup sum.  Every thread must call it.
@@ -150,12 +151,8 @@ __global__ __launch_bounds__(kScanThreads) void layout_windows(focus_layout_desc
   }
 }
 
-__global__ __launch_bounds__(kTokThreads) void layout_tokens(focus_layout_desc d, int32_t tiles) {
-  const int64_t gw = blockIdx.x / tiles;
-  const int64_t i = (int64_t)(blockIdx.x % tiles) * kTokThreads + threadIdx.x;
-  if (gw >= d.totals.n_windows) return;
-  const int64_t T = d.win_ntok[gw];
-  if (i >= T) return;
+// Token i of window gw (i < T_w checked by the caller).
+__device__ inline void layout_token(const focus_layout_desc& d, int64_t gw, int64_t i) {
   const int64_t n = d.win_nt[gw];
   const int64_t B = d.win_nsum[gw];
   const int64_t tok = d.win_tok_off[gw] + i;
@@ -201,6 +198,21 @@ __global__ __launch_bounds__(kTokThreads) void layout_tokens(focus_layout_desc d
   }
 }
 
+// One workgroup per (window, tile of kTokPerThread * kTokThreads tokens); a
+// thread places kTokPerThread tokens, kTokThreads apart, so the window's
+// descriptor loads are paid once per tile rather than once per token.
+__global__ __launch_bounds__(kTokThreads) void layout_tokens(focus_layout_desc d, int32_t tiles) {
+  const int64_t gw = blockIdx.x / tiles;
+  if (gw >= d.totals.n_windows) return;
+  const int64_t T = d.win_ntok[gw];
+  const int64_t i0 = (int64_t)(blockIdx.x % tiles) * kTokPerThread * kTokThreads + threadIdx.x;
+#pragma unroll
+  for (int r = 0; r < kTokPerThread; ++r) {
+    const int64_t i = i0 + (int64_t)r * kTokThreads;
+    if (i < T) layout_token(d, gw, i);
+  }
+}
+
 }  // namespace
 
 extern "C" focus_status focus_layout(const focus_layout_desc* d, focus_stream_t stream) {
@@ -227,7 +239,7 @@ extern "C" focus_status focus_layout(const focus_layout_desc* d, focus_stream_t 
   focus_status st = focus::launch_status();
   if (st != FOCUS_OK) return st;
   if (t.n_windows > 0 && t.max_window_tokens > 0) {
-    const int64_t tiles = focus::ceil_div(t.max_window_tokens, kTokThreads);
+    const int64_t tiles = focus::ceil_div(t.max_window_tokens, (int64_t)kTokThreads * kTokPerThread);
     const int64_t blocks = t.n_windows * tiles;
     if (blocks > INT32_MAX) return FOCUS_E_SHAPE;
     hipLaunchKernelGGL(layout_tokens, dim3((uint32_t)blocks), dim3(kTokThreads), 0, s, *d,
