@@ -684,32 +684,39 @@ __global__ __launch_bounds__(512, 2) void attn_ct(
       reinterpret_cast<const __bf16*>(d.cache_k) + ((int64_t)b * d.cache_cap * Hkv + hk) * D);
   const char* vcache = reinterpret_cast<const char*>(
       reinterpret_cast<const __bf16*>(d.cache_v) + ((int64_t)b * d.cache_cap * Hkv + hk) * D);
-  // Copy sources: tile tg starts at (tg < nct ? cache : window - nct tiles) +
-  // tg tiles.  Wave copy i of a tile (K and V) into (kbuf, vbuf); a partial
-  // tile (the last of a phase) clamps its rows to the last valid one.
+  // Key stream: nct cache tiles, then the window tiles.  The cache tiles start
+  // pad = 64 nct - C_w rows before cache row 0, so the one partial cache tile
+  // is tile 0 (its first pad rows are not keys) and every later tile up to
+  // the block's diagonal is full and unmasked.  Copy sources: tile tg starts
+  // at (tg < nct ? cache - pad rows : window - nct tiles) + tg tiles.  Wave
+  // copy i of a tile (K and V) into (kbuf, vbuf); a partial tile clamps its
+  // rows into [lo, last], the valid ones.
+  const int pad = nct * C::kBK - Cw;
   const int64_t tstride = (int64_t)C::kBK * row_bytes;
+  const char* kcache_b = kcache - (int64_t)pad * row_bytes;
+  const char* vcache_b = vcache - (int64_t)pad * row_bytes;
   const char* kwin_b = kwin - nct * tstride;
   const char* vwin_b = vwin - nct * tstride;
-  const int cfull = Cw / C::kBK;               // cache tiles below this are full
   const int wfull = nct + nwk / C::kBK;        // window tiles in [nct, wfull) are full
   struct Src {
     const char* k;
     const char* v;
-    uint32_t last;  // byte offset of the tile's last valid row (partial tiles)
+    uint32_t lo, last;  // byte offsets of the tile's first and last valid rows
     bool full;
   };
   auto tile_src = [&](int u) __attribute__((always_inline)) {
     const int tg = tb + u;
     const bool in_cache = tg < nct;
     Src r;
-    r.k = (in_cache ? kcache : kwin_b) + tg * tstride;
-    r.v = (in_cache ? vcache : vwin_b) + tg * tstride;
-    r.full = tg < cfull || (tg >= nct && tg < wfull);
-    r.last = (uint32_t)((in_cache ? Cw : nwk) - 1 - (in_cache ? tg : tg - nct) * C::kBK) * row_bytes;
+    r.k = (in_cache ? kcache_b : kwin_b) + tg * tstride;
+    r.v = (in_cache ? vcache_b : vwin_b) + tg * tstride;
+    r.full = in_cache ? (tg > 0 || pad == 0) : tg < wfull;
+    r.lo = (uint32_t)(in_cache && tg == 0 ? pad : 0) * row_bytes;
+    r.last = (uint32_t)(in_cache ? C::kBK - 1 : min(C::kBK, nwk - (tg - nct) * C::kBK) - 1) * row_bytes;
     return r;
   };
   auto issue = [&](const Src& sr, char* kbuf, char* vbuf, int i, bool clamp) __attribute__((always_inline)) {
-    const uint32_t rb = clamp ? min(rowb[i], sr.last) : rowb[i];
+    const uint32_t rb = clamp ? min(max(rowb[i], sr.lo), sr.last) : rowb[i];
     const char* ks = sr.k + (rb + kchunk[i]);
     const char* vs = sr.v + (rb + vchunk[i]);
     char* kl = kbuf + (wave * C::kDma + i) * 1024;
@@ -719,15 +726,15 @@ __global__ __launch_bounds__(512, 2) void attn_ct(
   };
 
   // Sub-tile j (32 keys) = half j & 1 of local tile j >> 1, i.e. global
-  // sub-tile J = 2 tb + j: cache rows [32 J, 32 J + 32) while J < 2 nct, then
-  // window rows from 32 (J - 2 nct).  This wave computes sub-tiles j < jlive
-  // (the window rows past its last query are skipped; the cache half-tile
-  // past C_w, if any, is computed fully masked).
+  // sub-tile J = 2 tb + j: stream rows [32 J, 32 J + 32), cache row
+  // 32 J + r - pad while J < 2 nct, then window row 32 (J - 2 nct) + r.  This
+  // wave computes sub-tiles j < jlive (the window rows past its last query
+  // are skipped).  Masks: the rows of tile 0 below pad, and the window rows
+  // past the query (from the wave's first diagonal sub-tile, wmask, on).
   const int J0 = 2 * tb;
   const int jlive = wave_live ? min(2 * (tb + ntiles), 2 * nct + (wq_hi >> 5) + 1) - J0 : 0;
-  const int cmask = Cw >> 5;                   // cache sub-tiles from here on reach past C_w
-  const int wmask = 2 * nct + (wq_lo >> 5);    // window sub-tiles from here on reach the diagonal
-  auto need_mask = [&](int J) { return (J >= cmask && J < 2 * nct) || J >= wmask; };
+  const int wmask = 2 * nct + (wq_lo >> 5);
+  auto need_mask = [&](int J) { return 32 * J < pad || J >= wmask; };
 
   // LDS operand offsets (lane parts; buffers and sub-tile rows are immediates).
   // K row 32 half + l32, chunk 2 s + g sits at chunk (2 s + g) ^ (l32 mod kCh16).
@@ -814,11 +821,17 @@ __global__ __launch_bounds__(512, 2) void attn_ct(
       const int J = J0 + j;
       if (!fast && need_mask(J)) {
         // s[v] = score of query qi with sub-tile key 8 (v/4) + 4 g + v%4
-        const bool c = J < 2 * nct;
-        const int lim_g = (c ? Cw - 32 * J - 1 : qi - 32 * (J - 2 * nct)) - 4 * g;
+        if (J < 2 * nct) {
+          const int lo_g = pad - 32 * J - 4 * g;  // rows of tile 0 before cache row 0
 #pragma unroll
-        for (int v = 0; v < 16; ++v)
-          if ((v >> 2) * 8 + (v & 3) > lim_g) s[v] = -INFINITY;
+          for (int v = 0; v < 16; ++v)
+            if ((v >> 2) * 8 + (v & 3) < lo_g) s[v] = -INFINITY;
+        } else {
+          const int lim_g = qi - 32 * (J - 2 * nct) - 4 * g;
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            if ((v >> 2) * 8 + (v & 3) > lim_g) s[v] = -INFINITY;
+        }
       }
       float mx = s[0];
 #pragma unroll
@@ -873,21 +886,22 @@ __global__ __launch_bounds__(512, 2) void attn_ct(
     __builtin_amdgcn_s_barrier();
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
   };
-  // step u: sub-tiles 2u, 2u + 1 from tile u (buffers kc/vc); K of tile u + 1
-  // (kn); copies of tile u + 3 into (kcp, vcp), the buffers tile u - 1 left.
   // step u: sub-tiles 2u, 2u + 1 from tile u (V in vc); K of tile u + 1
   // (kn); copies of tile u + 3 into (kcp, vcp), the buffers tile u - 1 left.
-  // A clean step (fast = true) is one of the leading cache steps: every
-  // sub-tile live and unmasked, the copied tile a full cache tile; it runs
-  // without any branch but the softmax's rescaling test.
+  // A clean step (fast = true) has every sub-tile live and unmasked for every
+  // wave and copies a full tile; it runs without any branch but the softmax's
+  // rescaling test.
   auto step = [&](int u, const char* vc, const char* kn, char* kcp, char* vcp, const bool fast)
       __attribute__((always_inline)) {
     pin_offsets();
     Src src;
     if (fast) {
-      const int64_t off = (int64_t)(tb + u + 3) * tstride;
-      src.k = kcache + off;
-      src.v = vcache + off;
+      const int tg = tb + u + 3;
+      const int64_t off = (int64_t)tg * tstride;
+      const bool c = tg < nct;
+      src.k = (c ? kcache_b : kwin_b) + off;
+      src.v = (c ? vcache_b : vwin_b) + off;
+      src.lo = 0;
       src.last = 0;
       src.full = true;
     } else {
@@ -903,28 +917,53 @@ __global__ __launch_bounds__(512, 2) void attn_ct(
   // using it here puts the wait for that load before the loop instead of
   // (conservatively) at the top of every iteration.
   asm volatile("" ::"v"(sc));
+  // Clean steps: tiles tb + u fully visible to the block's first query (the
+  // cache tiles past a partial tile 0, the window tiles below the block's
+  // rows) whose copy, tile u + 3, is a full tile; they form one run
+  // [u0, u1).  Tile u sits in stage (u - u0) mod 4, so the run starts on stage
+  // 0; a partial tile 0 (u0 = 1) takes stage 3 and the general step.  The
+  // run goes in rounds of four, its last (u1 - u0) mod 4 steps and the
+  // diagonal band after it in the general loop.
+  const int u0 = (tb == 0 && pad > 0 && ntiles > 0) ? 1 : 0;
+  const int u1 = max(u0, min(min(nct + (q0 + 1) / C::kBK, wfull - 3) - tb, ntiles - 3));
+  const int nclean = (u1 - u0) & ~3;
   // prologue: tiles 0..2 in flight, wait for 0 and 1
   {
     const Src s0 = tile_src(0), s1 = tile_src(1), s2 = tile_src(2);
+    if (u0 == 0) {
 #pragma unroll
-    for (int i = 0; i < C::kDma; ++i) {
-      if (ntiles > 0) issue(s0, kb0, vb0, i, !s0.full);
-      if (ntiles > 1) issue(s1, kb1, vb1, i, !s1.full);
-      if (ntiles > 2) issue(s2, kb2, vb2, i, !s2.full);
+      for (int i = 0; i < C::kDma; ++i) {
+        if (ntiles > 0) issue(s0, kb0, vb0, i, !s0.full);
+        if (ntiles > 1) issue(s1, kb1, vb1, i, !s1.full);
+        if (ntiles > 2) issue(s2, kb2, vb2, i, !s2.full);
+      }
+      wait_copies(ntiles > 2);
+      read_k(kb0, 0);
+      if (0 < jlive) qk(sacc[0]);
+      read_k(kb0, 1);
+    } else {
+#pragma unroll
+      for (int i = 0; i < C::kDma; ++i) {
+        issue(s0, kb3, vb3, i, true);
+        if (ntiles > 1) issue(s1, kb0, vb0, i, !s1.full);
+        if (ntiles > 2) issue(s2, kb1, vb1, i, !s2.full);
+      }
+      wait_copies(ntiles > 2);
+      read_k(kb3, 0);
+      if (0 < jlive) qk(sacc[0]);
+      read_k(kb3, 1);
     }
   }
-  wait_copies(ntiles > 2);
-  read_k(kb0, 0);
-  if (0 < jlive) qk(sacc[0]);
-  read_k(kb0, 1);
   // Let every scalar load land before the loop (lgkmcnt(0) once): a scalar
   // load still pending there would make the compiler wait for all LDS reads
   // at every counter wait inside the loop.
   __builtin_amdgcn_s_waitcnt(0xC07F);
-  // clean steps (a multiple of four, so the general loop starts at stage 0)
-  const int nclean = max(0, min(cfull - tb, ntiles) - 3) & ~3;
   int u = 0;
-  for (; u < nclean; u += 4) {
+  if (u0 > 0) {
+    step(0, vb3, kb0, kb2, vb2, false);
+    u = 1;
+  }
+  for (; u < u0 + nclean; u += 4) {
     step(u, vb0, kb1, kb3, vb3, true);
     step(u + 1, vb1, kb2, kb0, vb0, true);
     step(u + 2, vb2, kb3, kb1, vb1, true);
