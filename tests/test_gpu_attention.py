@@ -2,7 +2,7 @@
 
 Small cases compare every output row (several 128-row query tiles and 64-key
 tiles, ragged tails, GQA, head_dim 64 and 128, k = 0 windows, empty
-sequences); the workloads at full size run the very launch the benchmark times
+sequences, cache lengths on and around the key-tile edges); the workloads at full size run the very launch the benchmark times
 (every window of every sequence in one masked-parallel launch) and compare
 sampled windows and heads; the dense 32 kb point compares sampled rows.
 Properties checked on the device output: streaming (one window per call, the
@@ -117,6 +117,26 @@ def test_small_all_rows(case, dtype):
     p = Prefill(seq, W, km, H, Hkv, D, dtype, seed=1000 + case)
     ref = build_layout(seq, W, km)
     compare_windows(ref, p, range(ref["n_windows"]), list(range(H)), f"case {case} {dtype}")
+
+
+# Per-window cadences whose cache lengths C_w land on and around the 64-key
+# tile edges (0, 1, 32, 33, 63, 64, 65, 124-126): the partial cache tile is the
+# first key tile, masked below its first cache row, and every full tile after
+# it up to the block's diagonal takes the branch-free path.  One window has no
+# summaries (k = 0) and the last is truncated.
+EDGE_W = 640
+EDGE_KMER = [640, 21, 640, 22, 640, 640, 11, 640, 640, 9, 0, 100]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_cache_lengths_at_tile_edges(dtype):
+    seq = [EDGE_W * len(EDGE_KMER) - 37]
+    km = np.array(EDGE_KMER, np.int32)
+    ref = build_layout(seq, EDGE_W, km)
+    assert [int(c) for c in ref["win_cache_off"][:10]] == [0, 1, 32, 33, 63, 64, 65, 124, 125, 126]
+    announce(f"attn cache lengths at tile edges dtype={dtype}")
+    p = Prefill(seq, EDGE_W, km, 2, 1, 128, dtype, seed=77)
+    compare_windows(ref, p, range(ref["n_windows"]), [0, 1], f"tile edges {dtype}")
 
 
 def test_tiny_workload_f32_full():
