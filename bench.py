@@ -21,7 +21,10 @@ Also reported on the same JSON line:
                 the same 1 Mb prefill under the k-mer-local mask (HBM-bound), the
                 fidelity metrics over 1 M positions (HBM-bound), the FOCUS
                 adapter update of the summary tokens at 1 Mb (d_model 4096), and
-                the fused Q/K/V projection + RoPE + cache write at 1 Mb
+                the fused Q/K/V projection + RoPE + cache write at 1 Mb; as
+                context, what plain PyTorch ops reach on the same chip (HBM
+                read / write / copy, and a bf16 torch.matmul on the matrix
+                cores)
 """
 
 from __future__ import annotations
@@ -463,6 +466,29 @@ def secondary_hbm_reference(torch, nbytes=4 << 30, reps=10):
             "note": "torch.amax over rows (read), fill_ (write), copy_ (read + write) of 4 GiB"}
 
 
+def secondary_mfma_reference(torch, m=262144, n=4096, k=4096, reps=10):
+    """What the vendor GEMM (torch.matmul on bf16, hipBLASLt) reaches on this
+    box's matrix cores under the same power limit (context for the MFMA-bound
+    kernels' fractions; not part of the hot path)."""
+    a = torch.empty(m, k, dtype=torch.bfloat16, device="cuda:0").normal_()
+    b = (torch.empty(k, n, device="cuda:0").normal_() / 64).to(torch.bfloat16)
+    c = torch.empty(m, n, dtype=torch.bfloat16, device="cuda:0")
+    torch.matmul(a, b, out=c)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        torch.matmul(a, b, out=c)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del a, b, c
+    torch.cuda.empty_cache()
+    tf = 2.0 * m * n * k / (ms * 1e-3) / 1e12
+    return {"gemm": f"{m} x {n} x {k} bf16 (torch.matmul)", "ms": ms, "tflops": tf,
+            "frac_mfma": tf * 1e12 / PEAK_BF16_FLOPS}
+
+
 def secondary_decode(torch, F, fw, steps=None):
     """Batch-16 decode at ~1 Mb: 10 000 cached summaries plus a partial window.
     A step is the device schedule (the next token's kind) + focus_decode_step."""
@@ -832,6 +858,8 @@ def main():
         sec = {"compaction_1mb": secondary_compaction(torch, F, s, timer)}
         log("secondary: HBM reference")
         sec["hbm_reference"] = secondary_hbm_reference(torch)
+        log("secondary: MFMA reference")
+        sec["mfma_reference"] = secondary_mfma_reference(torch)
         log("secondary: streaming")
         sec["streaming_1mb"] = secondary_streaming(torch, F, s)
         log("secondary: k-mer-local mask")
