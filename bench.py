@@ -163,15 +163,18 @@ class ClockSampler:
         return False
 
     def summary(self):
-        # samples taken while the clock is up (the GPU busy), not idle ones
-        busy = [c for c in self.samples if c[0] > 500]
+        # samples taken while the clock is up (the GPU busy: above 1 GHz; the
+        # idle clock reads ~0.5 GHz, e.g. between launches), not idle ones
+        busy = [c for c in self.samples if c[0] > 1000]
         if not self.ok or not busy:
             return {"unavailable": self.error or f"{len(self.samples)} samples, none with the clock up"}
         clk = np.array([c[0] for c in busy])
         pw = np.array([c[1] for c in busy])
-        return {"gfxclk_MHz_mean": float(clk.mean()), "gfxclk_MHz_min": float(clk.min()),
+        return {"gfxclk_MHz_median": float(np.median(clk)), "gfxclk_MHz_mean": float(clk.mean()),
+                "gfxclk_MHz_min": float(clk.min()), "gfxclk_MHz_max": float(clk.max()),
                 "socket_power_W_mean": float(np.nanmean(pw)) if np.isfinite(pw).any() else None,
-                "samples": len(busy), "source": "amdsmi GPU metrics (current_gfxclks, current_socket_power)"}
+                "samples": len(busy), "samples_idle": len(self.samples) - len(busy),
+                "source": "amdsmi GPU metrics (current_gfxclks, current_socket_power)"}
 
 
 def prefill_setup(torch, F, fw, w):
