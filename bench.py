@@ -62,10 +62,17 @@ def log(msg):
 
 
 def source_hash(paths):
+    """Hash of the code of the given sources: comments and whitespace are
+    dropped, so editing a comment does not retire counters taken on the same
+    code."""
+    import re
     h = hashlib.sha256()
     for p in paths:
-        with open(os.path.join(ROOT, p), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, p)) as f:
+            t = f.read()
+        t = re.sub(r"/\*.*?\*/", " ", t, flags=re.S)
+        t = re.sub(r"//[^\n]*", "", t)
+        h.update(" ".join(t.split()).encode())
     return h.hexdigest()[:16]
 
 

@@ -29,6 +29,9 @@
 //   O^T += V^T P^T  the same MFMA; P comes straight from the S^T accumulator
 //                 (rounded to bf16), V^T is read from LDS with the gfx950
 //                 transposing read ds_read_b64_tr_b16.
+// The cache's tiles start 64 ceil(C_w / 64) - C_w rows before cache row 0, so
+// its one partial tile is the first key tile and every tile from there to the
+// block's diagonal is full and unmasked: those steps run a branch-free body.
 // Both LDS tiles are XOR-swizzled so that the MFMA operand reads are free of
 // bank conflicts.  Blocks are dealt out so that all query tiles of one
 // (window, head) land on the same XCD (sharing K/V through its L2) and the
