@@ -31,3 +31,16 @@ def test_one_mb_counts():
     # per window of 1 010 tokens: ten 101-token k-mers, plus the boundary after the first
     per_win = 10 * (101 * 102 // 2) + 101 * (10 * 9 // 2)
     assert bench.kmer_local_pairs(lay["win_ntok"], lay["win_cache_off"], 100) == 1000 * per_win + 999 * 1010
+
+
+def test_traffic_record_keyed_to_code_not_comments(tmp_path, monkeypatch):
+    """The counter record's source hash covers the attention's code: a comment
+    or whitespace edit keeps it, any code edit changes it."""
+    src = tmp_path / "k.hip"
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    src.write_text("int f(int x) {\n  return x + 1;  // one\n}\n/* block */\n")
+    h0 = bench.source_hash(["k.hip"])
+    src.write_text("// header\nint f(int x) {\n    return x + 1;  /* other */\n}\n")
+    assert bench.source_hash(["k.hip"]) == h0
+    src.write_text("int f(int x) {\n  return x + 2;  // one\n}\n")
+    assert bench.source_hash(["k.hip"]) != h0
