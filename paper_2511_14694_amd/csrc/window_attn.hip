@@ -38,9 +38,10 @@
 // listed windows are started in list order (last window = largest cache first
 // by default).
 //
-// The k-mer-local mask (attn_bf16<D, 4, true, false>) uses the same MFMA
-// scheme without the software pipeline: 4 waves, each copying its share of
-// 32-key tiles through four LDS stages.
+// The k-mer-local mask (attn_kl) uses the same MFMA scheme without the
+// software pipeline: one workgroup of 4 waves streams all query tiles of a
+// (window, head), each wave copying its share of 32-key tiles through five
+// LDS stages.
 //
 // Summary queries (the FOCUS adapter's attention): under C(t) several windows'
 // summaries share one workgroup (attn_sq_block); otherwise the bf16 kernel
@@ -67,10 +68,9 @@ constexpr float kLazy = 8.0f;       // rescale when the max grows by > 2^8
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 typedef __attribute__((address_space(3))) void lds_void;
 
-// Waves per workgroup of the bf16 kernel (each wave owns 32 query rows):
+// Waves per workgroup of the bf16 kernels (each wave owns 32 query rows):
 // eight under C(t), where a workgroup streams thousands of keys; four under the
-// k-mer-local mask, where it visits a handful of tiles and two workgroups per
-// CU hide each other's start-up.
+// k-mer-local mask (attn_kl), where a query tile visits a handful of key tiles.
 constexpr int kBf16Waves = 8;
 constexpr int kBf16WavesKL = 4;
 
@@ -202,28 +202,21 @@ struct Split {
 };
 constexpr Split kNoSplit = {1, nullptr, nullptr, 0, 0};
 
-// The k-mer-local and summary-query modes (the C(t) window attention is
-// attn_ct below).
-//
-// The k-mer-local window attention (KL, not SQ) visits only a handful of
-// tiles per workgroup (the summary list and the window rows of its k-mers),
-// so it is bound by the latency of each tile's copy: it takes 32-key tiles
-// through four LDS stages, three tiles in flight while one is computed (64 KB,
-// two workgroups per compute unit).  The summary-query mode keeps 64-key
-// tiles through two stages.
+// Summary queries (the FOCUS adapter's attention) under C(t) (KL false) or
+// the k-mer-local mask (KL true), where attn_sq_block does not apply: W waves
+// of 32 summary slots per (window, head), 64-key tiles through two LDS stages.
+// (The window attention itself is attn_ct under C(t) and attn_kl under the
+// k-mer-local mask.)
 template <int D, int W, bool KL, bool SQ>
 __global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_desc d, float sc, int64_t n_pairs,
                                                                      int QT, SumQ sq) {
-  static_assert(KL || SQ, "C(t) window attention is attn_ct");
-  constexpr bool kDeep = KL && !SQ;
-  using C = Cfg<D, W, kDeep ? 32 : 64>;
+  static_assert(SQ, "the window attention is attn_ct (C(t)) or attn_kl (k-mer-local)");
+  using C = Cfg<D, W, 64>;
   // K and V tile buffers as separate arrays, referenced statically by a loop
   // unrolled by the stage count: the compiler can then tell a tile being read
   // from the ones being filled, and waits for the copies only where it must.
   __shared__ __attribute__((aligned(1024))) char kbuf0[C::kTile], kbuf1[C::kTile];
   __shared__ __attribute__((aligned(1024))) char vbuf0[C::kTile], vbuf1[C::kTile];
-  __shared__ __attribute__((aligned(1024))) char kbuf2[kDeep ? C::kTile : 16], kbuf3[kDeep ? C::kTile : 16];
-  __shared__ __attribute__((aligned(1024))) char vbuf2[kDeep ? C::kTile : 16], vbuf3[kDeep ? C::kTile : 16];
 
   const int tid = threadIdx.x;
   const Item it = map_block(blockIdx.x, n_pairs, d.n_heads, QT);
@@ -235,29 +228,22 @@ __global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_d
   }
   const int T = d.win_ntok[gw];
   const int q0 = it.qt * C::kBQ;
-  int nq = T;          // query slots of the window
-  int64_t s0 = 0;      // summary mode: the window's first summary
-  if constexpr (SQ) {
-    nq = sq.win_nsum[gw];
-    s0 = sq.win_sum_off[gw];
-  }
+  const int nq = sq.win_nsum[gw];        // query slots of the window: its summaries
+  const int64_t s0 = sq.win_sum_off[gw];  // the window's first summary
   if (q0 >= nq) return;
   const int Cw = d.win_cache_off[gw];
   const int b = d.win_seq[gw];
   const int64_t tok0 = d.win_tok_off[gw] - d.qkv_tok_base;
-  if (b < 0 || b >= d.batch || Cw < 0 || Cw > d.cache_cap || tok0 < 0 || tok0 + T > d.qkv_rows ||
-      (SQ && (nq > T || s0 < sq.base || s0 + nq > sq.base + sq.rows))) {
+  if (b < 0 || b >= d.batch || Cw < 0 || Cw > d.cache_cap || tok0 < 0 || tok0 + T > d.qkv_rows || nq > T ||
+      s0 < sq.base || s0 + nq > sq.base + sq.rows) {
     if (tid == 0) focus::raise_err(d.err, FOCUS_ERR_BOUNDS);
     return;
   }
   // window row of query slot j (clamped to the last slot)
   auto qpos = [&](int j) -> int {
     j = min(j, nq - 1);
-    if constexpr (SQ) {
-      const int64_t r = sq.sum_tok[s0 + j] - d.win_tok_off[gw];
-      return (int)(r < 0 ? 0 : r >= T ? T - 1 : r);
-    }
-    return j;
+    const int64_t r = sq.sum_tok[s0 + j] - d.win_tok_off[gw];
+    return (int)(r < 0 ? 0 : r >= T ? T - 1 : r);
   };
   const int H = d.n_heads, Hkv = d.n_kv_heads, h = it.h;
   const int hk = h / (H / Hkv);
@@ -277,8 +263,7 @@ __global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_d
     }
     nsum = kw > 0 ? (T + kw) / (kw + 1) : 0;
     // first row of the k-mer of the tile's first query (summary j closes k-mer j)
-    const int first_kmer = SQ ? q0 : (kw > 0 ? q0 / (kw + 1) : 0);
-    tw0 = kw > 0 ? first_kmer * (kw + 1) / C::kBK : 0;
+    tw0 = kw > 0 ? q0 * (kw + 1) / C::kBK : 0;
   }
   const int nct = KL ? (nsum + C::kBK) / C::kBK : (Cw + C::kBK - 1) / C::kBK;
   const int nwt = (nwk + C::kBK - 1) / C::kBK - tw0;
@@ -287,26 +272,25 @@ __global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_d
 
   const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, g = lane >> 5;
   const int js = q0 + wave * 32 + l32;  // this lane's query slot
-  const int qi = SQ ? qpos(js) : js;     // and its row inside the window
-  const int wq_lo = qpos(q0 + wave * 32), wq_hi = SQ ? qpos(q0 + wave * 32 + 31) : wq_lo + 31;
+  const int qi = qpos(js);              // and its row inside the window
+  const int wq_lo = qpos(q0 + wave * 32), wq_hi = qpos(q0 + wave * 32 + 31);
   const bool wave_live = q0 + wave * 32 < nq;
   // k-mer-local: this lane's k-mer index jq inside the window and that
   // k-mer's first row qlo; klo_w: first row of the wave's first k-mer.
   int jq = 0, qlo = 0, klo_w = 0;
   if constexpr (KL) {
     if (kw > 0) {
-      jq = SQ ? min(js, nq - 1) : qi / (kw + 1);
+      jq = min(js, nq - 1);
       qlo = jq * (kw + 1);
-      klo_w = (SQ ? min(q0 + wave * 32, nq - 1) : wq_lo / (kw + 1)) * (kw + 1);
+      klo_w = min(q0 + wave * 32, nq - 1) * (kw + 1);
     }
   }
 
   // Q^T as the B operand: lane holds query l32, head_dim [16s + 8g, 16s + 8g + 8).
   bf16x8 qf[C::kKsteps];
   {
-    const int64_t qrow = SQ ? s0 + min(js, nq - 1) - sq.base : tok0 + min(qi, T - 1);
-    const bf16x8* qp = reinterpret_cast<const bf16x8*>(
-        reinterpret_cast<const __bf16*>(SQ ? sq.q : d.q) + (qrow * H + h) * D);
+    const int64_t qrow = s0 + min(js, nq - 1) - sq.base;
+    const bf16x8* qp = reinterpret_cast<const bf16x8*>(reinterpret_cast<const __bf16*>(sq.q) + (qrow * H + h) * D);
 #pragma unroll
     for (int s = 0; s < C::kKsteps; ++s) qf[s] = qp[2 * s + g];
   }
@@ -502,62 +486,24 @@ __global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_d
     }
   };
 
-  if constexpr (kDeep) {
-    // Step u: copies of tile u + 3 into the stage tile u - 1 left, tile u
-    // computed, then this wave waits until its copies of tile u + 1 have
-    // landed (those of u + 2 and u + 3 may stay in flight) and the barrier
-    // makes that true for every wave's share.
-    constexpr int kPer = 2 * kDma;  // copies a wave issues per tile
-    auto wait_next = [&](int u) __attribute__((always_inline)) {
-      const int younger = max(0, min(2, ntiles - 2 - u));  // tiles u + 2, u + 3 issued
-      __atomic_signal_fence(__ATOMIC_SEQ_CST);
-      if (younger == 2)
-        __builtin_amdgcn_s_waitcnt(((2 * kPer) & 15) | (((2 * kPer) >> 4) << 14) | (7 << 4) | (15 << 8));
-      else if (younger == 1)
-        __builtin_amdgcn_s_waitcnt((kPer & 15) | ((kPer >> 4) << 14) | (7 << 4) | (15 << 8));
-      else
-        __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
-      __builtin_amdgcn_s_barrier();
-      __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    };
-    auto step = [&](int u, const char* kc, const char* vc, char* kn, char* vn) __attribute__((always_inline)) {
-      if (u + 3 < ntiles) issue_tile(u + 3, kn, vn);
-      compute_tile(u, kc, vc);
-      wait_next(u);
-    };
-    issue_tile(0, kbuf0, vbuf0);
-    if (1 < ntiles) issue_tile(1, kbuf1, vbuf1);
-    if (2 < ntiles) issue_tile(2, kbuf2, vbuf2);
-    wait_next(-1);  // tile 0 has landed
-    for (int t = 0; t < ntiles; t += 4) {
-      step(t, kbuf0, vbuf0, kbuf3, vbuf3);
-      if (t + 1 >= ntiles) break;
-      step(t + 1, kbuf1, vbuf1, kbuf0, vbuf0);
-      if (t + 2 >= ntiles) break;
-      step(t + 2, kbuf2, vbuf2, kbuf1, vbuf1);
-      if (t + 3 >= ntiles) break;
-      step(t + 3, kbuf3, vbuf3, kbuf2, vbuf2);
-    }
-  } else {
-    // The barrier closing each step also waits for the next tile's copies.
-    issue_tile(0, kbuf0, vbuf0);
+  // The barrier closing each step also waits for the next tile's copies.
+  issue_tile(0, kbuf0, vbuf0);
+  __syncthreads();
+  for (int t = 0; t < ntiles; t += 2) {
+    if (t + 1 < ntiles) issue_tile(t + 1, kbuf1, vbuf1);
+    compute_tile(t, kbuf0, vbuf0);
     __syncthreads();
-    for (int t = 0; t < ntiles; t += 2) {
-      if (t + 1 < ntiles) issue_tile(t + 1, kbuf1, vbuf1);
-      compute_tile(t, kbuf0, vbuf0);
-      __syncthreads();
-      if (t + 1 >= ntiles) break;
-      if (t + 2 < ntiles) issue_tile(t + 2, kbuf0, vbuf0);
-      compute_tile(t + 1, kbuf1, vbuf1);
-      __syncthreads();
-    }
+    if (t + 1 >= ntiles) break;
+    if (t + 2 < ntiles) issue_tile(t + 2, kbuf0, vbuf0);
+    compute_tile(t + 1, kbuf1, vbuf1);
+    __syncthreads();
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
-  if (SQ ? js < nq : qi < T) {
+  if (js < nq) {
     const float inv = 1.f / l_tot;
-    const int64_t orow = SQ ? s0 + js - sq.base : tok0 + qi;
-    __bf16* op = reinterpret_cast<__bf16*>(SQ ? sq.o : d.o) + (orow * H + h) * D;
+    const int64_t orow = s0 + js - sq.base;
+    __bf16* op = reinterpret_cast<__bf16*>(sq.o) + (orow * H + h) * D;
 #pragma unroll
     for (int dt = 0; dt < C::kDtiles; ++dt)
 #pragma unroll
@@ -568,9 +514,452 @@ __global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_d
         w.y = focus::pack_bf16x2(oacc[dt][4 * v4 + 2] * inv, oacc[dt][4 * v4 + 3] * inv);
         *reinterpret_cast<uint2*>(op + 32 * dt + 8 * v4 + 4 * g) = w;
       }
-    float* lse = SQ ? sq.lse : d.lse;
-    if (g == 0 && lse) lse[orow * H + h] = (m_run + log2f(l_tot)) * kLn2;
+    if (g == 0 && sq.lse) sq.lse[orow * H + h] = (m_run + log2f(l_tot)) * kLn2;
   }
+}
+
+// ------------------------------------------------- bf16 MFMA, k-mer-local
+
+// q[s] = p[2 s] (16 bytes each, 32 bytes apart) for s < NS, returned only once
+// every vector memory operation of this wave has completed (the wait is part
+// of the statement, so the compiler tracks no load in flight into q).
+// The k-mer-local kernel below issues its global -> LDS copies as inline
+// assembly, so the compiler does not track them: with the compiler-visible
+// copy in this loop's control flow it conservatively waits for every copy in
+// flight before a step's LDS reads, which would leave one tile in flight
+// instead of three.  The kernel's own waits (a vmcnt wait and a barrier that
+// close each step) order every LDS read after the copies it needs.
+//
+// 16 bytes per lane from src to LDS byte lds + 16 lane (one wave: 1 KB).
+__device__ __forceinline__ void copy_to_lds(const void* src, uint32_t lds) {
+  asm volatile(
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, off"
+      :
+      : "v"(src), "{m0}"(lds)
+      : "memory");
+}
+__device__ __forceinline__ uint32_t lds_addr(const char* p) {
+  typedef const __attribute__((address_space(3))) char lds_char;
+  return (uint32_t)(uintptr_t)(lds_char*)p;
+}
+
+template <int NS>
+__device__ __forceinline__ void load_q_now(const bf16x8* p, bf16x8 (&q)[NS]) {
+  static_assert(NS == 4 || NS == 8, "head_dim 64 or 128");
+  u32x4 r[NS];
+  if constexpr (NS == 8) {
+    asm volatile(
+        "global_load_dwordx4 %0, %8, off\n\t"
+        "global_load_dwordx4 %1, %8, off offset:32\n\t"
+        "global_load_dwordx4 %2, %8, off offset:64\n\t"
+        "global_load_dwordx4 %3, %8, off offset:96\n\t"
+        "global_load_dwordx4 %4, %8, off offset:128\n\t"
+        "global_load_dwordx4 %5, %8, off offset:160\n\t"
+        "global_load_dwordx4 %6, %8, off offset:192\n\t"
+        "global_load_dwordx4 %7, %8, off offset:224\n\t"
+        "s_waitcnt vmcnt(0)"
+        : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]), "=&v"(r[7])
+        : "v"(p)
+        : "memory");
+  } else {
+    asm volatile(
+        "global_load_dwordx4 %0, %4, off\n\t"
+        "global_load_dwordx4 %1, %4, off offset:32\n\t"
+        "global_load_dwordx4 %2, %4, off offset:64\n\t"
+        "global_load_dwordx4 %3, %4, off offset:96\n\t"
+        "s_waitcnt vmcnt(0)"
+        : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3])
+        : "v"(p)
+        : "memory");
+  }
+#pragma unroll
+  for (int s = 0; s < NS; ++s) q[s] = __builtin_bit_cast(bf16x8, r[s]);
+}
+
+// The same loads without the wait: q is written when the loads land.  The
+// compiler sees q as written here, so nothing may read, copy or spill it
+// before wait_loaded (below) has run; the kernel reads it only after that.
+template <int NS>
+__device__ __forceinline__ void load_q_async(const bf16x8* p, bf16x8 (&q)[NS]) {
+  static_assert(NS == 4 || NS == 8, "head_dim 64 or 128");
+  u32x4 r[NS];
+  if constexpr (NS == 8) {
+    asm volatile(
+        "global_load_dwordx4 %0, %8, off\n\t"
+        "global_load_dwordx4 %1, %8, off offset:32\n\t"
+        "global_load_dwordx4 %2, %8, off offset:64\n\t"
+        "global_load_dwordx4 %3, %8, off offset:96\n\t"
+        "global_load_dwordx4 %4, %8, off offset:128\n\t"
+        "global_load_dwordx4 %5, %8, off offset:160\n\t"
+        "global_load_dwordx4 %6, %8, off offset:192\n\t"
+        "global_load_dwordx4 %7, %8, off offset:224"
+        : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]), "=&v"(r[7])
+        : "v"(p)
+        : "memory");
+  } else {
+    asm volatile(
+        "global_load_dwordx4 %0, %4, off\n\t"
+        "global_load_dwordx4 %1, %4, off offset:32\n\t"
+        "global_load_dwordx4 %2, %4, off offset:64\n\t"
+        "global_load_dwordx4 %3, %4, off offset:96"
+        : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3])
+        : "v"(p)
+        : "memory");
+  }
+#pragma unroll
+  for (int s = 0; s < NS; ++s) q[s] = __builtin_bit_cast(bf16x8, r[s]);
+}
+
+// Wait until at most N of this wave's vector memory operations are
+// outstanding, as an update of q: reads of q cannot be scheduled before it.
+template <int N, int NS>
+__device__ __forceinline__ void wait_loaded(bf16x8 (&q)[NS]) {
+  static_assert(NS == 4 || NS == 8, "head_dim 64 or 128");
+  u32x4 r[NS];
+#pragma unroll
+  for (int s = 0; s < NS; ++s) r[s] = __builtin_bit_cast(u32x4, q[s]);
+  if constexpr (NS == 8) {
+    asm volatile("s_waitcnt vmcnt(%8)"
+                 : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]), "+v"(r[4]), "+v"(r[5]), "+v"(r[6]), "+v"(r[7])
+                 : "n"(N));
+  } else {
+    asm volatile("s_waitcnt vmcnt(%4)" : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]) : "n"(N));
+  }
+#pragma unroll
+  for (int s = 0; s < NS; ++s) q[s] = __builtin_bit_cast(bf16x8, r[s]);
+}
+
+// The k-mer-local window attention (Section 3.2 rule): one workgroup streams a
+// whole (window, head).  Its 4 waves x 32 rows take the window's 128-row query
+// tiles one after another, and the key tiles of all of them form one stream of
+// 32-key tiles through five LDS stages, four in flight while one is computed
+// (80 KB: two workgroups fill a compute unit's LDS).
+// Query tile q visits the gathered summary list [carried boundary ; the
+// window's summaries] and then the window tiles from the one holding the first
+// row of its first k-mer up to its last row, with a two-sided mask keeping each
+// row's own k-mer.  The copies run three tiles ahead across query-tile
+// boundaries (every step copies one tile; past the end of the stream the last
+// tile again, into a stage nobody reads any more, so every wait is the same),
+// and the next query tile's Q loads while this one is computed.  A workgroup
+// pays the start-up latency once per window rather than once per query tile.
+template <int D>
+__global__ __launch_bounds__(256, 2) void attn_kl(focus_attn_desc d, float sc, int64_t n_pairs) {
+  using C = Cfg<D, 4, 32>;
+  __shared__ __attribute__((aligned(1024))) char kb0[C::kTile], kb1[C::kTile], kb2[C::kTile], kb3[C::kTile], kb4[C::kTile];
+  __shared__ __attribute__((aligned(1024))) char vb0[C::kTile], vb1[C::kTile], vb2[C::kTile], vb3[C::kTile], vb4[C::kTile];
+
+  const int tid = threadIdx.x;
+  // Block -> (listed window, head), heads fastest: the workgroups running at
+  // one time read the same token rows of a few windows (each head its slice
+  // of every row), which HBM serves far better than one head's slice of many
+  // windows (10.7 vs 7.9 ms at 1 Mb).
+  if ((int64_t)blockIdx.x >= n_pairs) return;
+  Item it;
+  it.list_idx = (int64_t)blockIdx.x / d.n_heads;
+  it.h = (int)((int64_t)blockIdx.x % d.n_heads);
+  const int64_t gw = listed_window(d, it.list_idx);
+  if (gw < 0 || gw >= d.totals.n_windows) {
+    if (tid == 0) focus::raise_err(d.err, FOCUS_ERR_BOUNDS);
+    return;
+  }
+  const int T = d.win_ntok[gw];
+  if (T <= 0) return;
+  const int Cw = d.win_cache_off[gw];
+  const int b = d.win_seq[gw];
+  const int64_t tok0 = d.win_tok_off[gw] - d.qkv_tok_base;
+  const int kw = d.win_kmer ? d.win_kmer[gw] : d.kmer_uniform;
+  if (b < 0 || b >= d.batch || Cw < 0 || Cw > d.cache_cap || tok0 < 0 || tok0 + T > d.qkv_rows || kw < 0) {
+    if (tid == 0) focus::raise_err(d.err, FOCUS_ERR_BOUNDS);
+    return;
+  }
+  const int H = d.n_heads, Hkv = d.n_kv_heads, h = it.h;
+  const int hk = h / (H / Hkv);
+  const int nsum = kw > 0 ? (T + kw) / (kw + 1) : 0;
+  const int nct = (nsum + C::kBK) / C::kBK;  // tiles of the summary list (boundary + nsum)
+  const int nqt = (T + C::kBQ - 1) / C::kBQ;
+  // Query tile q: its first window tile (the one holding the first row of its
+  // first k-mer), the window keys it can see and its tile count.
+  auto tw0_of = [&](int q) { return kw > 0 ? q * C::kBQ / (kw + 1) * (kw + 1) / C::kBK : 0; };
+  auto nwk_of = [&](int q) { return min(q * C::kBQ + C::kBQ, T); };
+  auto ntiles_of = [&](int q) { return nct + (nwk_of(q) + C::kBK - 1) / C::kBK - tw0_of(q); };
+  int nsteps = 0;
+  for (int q = 0; q < nqt; ++q) nsteps += ntiles_of(q);
+
+  const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, g = lane >> 5;
+  constexpr int kRPK = 1024 / C::kRB;
+  constexpr int kDma = C::kTile / 1024 / C::kWaves;
+  static_assert(kDma >= 1 && C::kTile % (1024 * C::kWaves) == 0, "tile must split into 1 KB wave loads");
+  constexpr int kPer = 2 * kDma;  // copies a wave issues per tile
+  const uint32_t row_bytes = (uint32_t)(Hkv * D * 2);
+  uint32_t rowb[kDma], kchunk[kDma], vchunk[kDma];
+#pragma unroll
+  for (int i = 0; i < kDma; ++i) {
+    const int r = (wave * kDma + i) * kRPK + lane / C::kCh16;
+    const int p = lane % C::kCh16;
+    const int f = D == 128 ? (r & 3) : ((r >> 1) & 1);
+    rowb[i] = (uint32_t)r * row_bytes;
+    kchunk[i] = (uint32_t)((p ^ (r % C::kCh16)) * 16);
+    vchunk[i] = (uint32_t)((((p >> 2) ^ f) * 4 + (p & 3)) * 16);
+  }
+  const char* kwin = reinterpret_cast<const char*>(reinterpret_cast<const __bf16*>(d.k) + (tok0 * Hkv + hk) * D);
+  const char* vwin = reinterpret_cast<const char*>(reinterpret_cast<const __bf16*>(d.v) + (tok0 * Hkv + hk) * D);
+  const char* kcache = reinterpret_cast<const char*>(
+      reinterpret_cast<const __bf16*>(d.cache_k) + ((int64_t)b * d.cache_cap * Hkv + hk) * D);
+  const char* vcache = reinterpret_cast<const char*>(
+      reinterpret_cast<const __bf16*>(d.cache_v) + ((int64_t)b * d.cache_cap * Hkv + hk) * D);
+  const __bf16* qwin = reinterpret_cast<const __bf16*>(d.q) + (tok0 * H + h) * D;
+  __bf16* owin = reinterpret_cast<__bf16*>(d.o) + (tok0 * H + h) * D;
+
+  // Q^T of query tile q as the B operand: lane holds query row
+  // 128 q + 32 wave + l32 (clamped to the window), head_dim [16s + 8g, +8).
+  auto q_row = [&](int q) __attribute__((always_inline)) {
+    const int r = min(q * C::kBQ + wave * 32 + l32, T - 1);
+    return reinterpret_cast<const bf16x8*>(qwin + (int64_t)r * H * D) + g;
+  };
+
+  // Issue side: the next tile of the stream (query tile iq, its tile it_).
+  int iq = 0, it_ = 0, i_tw0 = tw0_of(0), i_nwk = nwk_of(0), i_nt = ntiles_of(0);
+  auto issue_next = [&](char* kbuf, char* vbuf) __attribute__((always_inline)) {
+    // Per-lane source rows of this wave's share, then one copy pair per 1 KB.
+    const char* ks[kDma];
+    const char* vs[kDma];
+    if (it_ < nct) {
+      // Summary-list entry R = 32 t + r: R = 0 is the carried boundary, R >= 1
+      // the window's summary R - 1 at window row R (k + 1) - 1 (the last one at
+      // T - 1).  Rows past the list repeat its last entry (masked).
+#pragma unroll
+      for (int i = 0; i < kDma; ++i) {
+        const int r = (wave * kDma + i) * kRPK + lane / C::kCh16;
+        const int R = min(it_ * C::kBK + r, nsum);
+        const bool boundary = R == 0 && Cw > 0;
+        const int wrow = R == 0 ? 0 : min(R * (kw + 1) - 1, T - 1);
+        ks[i] = (boundary ? kcache + (int64_t)(Cw - 1) * row_bytes : kwin + (int64_t)wrow * row_bytes) + kchunk[i];
+        vs[i] = (boundary ? vcache + (int64_t)(Cw - 1) * row_bytes : vwin + (int64_t)wrow * row_bytes) + vchunk[i];
+      }
+    } else {
+      const int row0 = (it_ - nct + i_tw0) * C::kBK;
+      const int nvalid = i_nwk - row0;
+      const char* kb = kwin + (int64_t)row0 * row_bytes;
+      const char* vb = vwin + (int64_t)row0 * row_bytes;
+      const uint32_t last = (uint32_t)(nvalid - 1) * row_bytes;
+#pragma unroll
+      for (int i = 0; i < kDma; ++i) {
+        const uint32_t rb = nvalid >= C::kBK ? rowb[i] : min(rowb[i], last);
+        ks[i] = kb + (rb + kchunk[i]);
+        vs[i] = vb + (rb + vchunk[i]);
+      }
+    }
+    const uint32_t kl = lds_addr(kbuf) + wave * kDma * 1024;
+    const uint32_t vl = lds_addr(vbuf) + wave * kDma * 1024;
+#pragma unroll
+    for (int i = 0; i < kDma; ++i) {
+      copy_to_lds(ks[i], kl + i * 1024);
+      copy_to_lds(vs[i], vl + i * 1024);
+    }
+    if (it_ + 1 < i_nt) {
+      ++it_;
+    } else if (iq + 1 < nqt) {
+      ++iq;
+      it_ = 0;
+      i_tw0 = tw0_of(iq);
+      i_nwk = nwk_of(iq);
+      i_nt = ntiles_of(iq);
+    }  // else: the stream has ended; the last tile is copied again
+  };
+
+  // Compute side: query tile cq, its tile ct; this lane's row qi, its k-mer
+  // index jq and that k-mer's first row qlo; klo_w: first row of the wave's
+  // first k-mer.
+  int cq = 0, ct = 0, c_tw0 = tw0_of(0), c_nt = ntiles_of(0);
+  int wq_lo = 0, qi = 0, jq = 0, qlo = 0, klo_w = 0;
+  bool wave_live = false;
+  auto set_q = [&](int q) __attribute__((always_inline)) {
+    wq_lo = q * C::kBQ + wave * 32;
+    qi = wq_lo + l32;
+    wave_live = wq_lo < T;
+    jq = kw > 0 ? qi / (kw + 1) : 0;
+    qlo = jq * (kw + 1);
+    klo_w = kw > 0 ? wq_lo / (kw + 1) * (kw + 1) : 0;
+  };
+
+  f32x16 oacc[C::kDtiles];
+#pragma unroll
+  for (int dt = 0; dt < C::kDtiles; ++dt)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) oacc[dt][v] = 0.f;
+  float m_run = kMinit, l_run = 0.f;
+  bf16x8 qf[C::kKsteps], qn[C::kKsteps];
+  const int grp = lane >> 4, ri = (lane >> 2) & 3, bq = lane & 3;
+
+  auto compute_tile = [&](const char* kl, const char* vl) __attribute__((always_inline)) {
+    const bool in_list = ct < nct;
+    const int row0 = in_list ? ct * C::kBK : (ct - nct + c_tw0) * C::kBK;
+    const bool live = wave_live && (in_list || (row0 <= wq_lo + 31 && row0 + C::kBK > klo_w));
+    // visible tile keys: lo <= kk <= lim
+    const int lim = in_list ? jq - row0 : qi - row0;
+    const int lo = in_list ? (Cw > 0 ? 0 : 1) - row0 : qlo - row0;
+    if (!live) return;
+    f32x16 sacc;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) sacc[v] = 0.f;
+    const int kx = g ^ (l32 & (C::kCh16 - 1));
+    auto kread = [&](int s) {
+      int ko = l32 * C::kRB + (((2 * s) ^ kx) << 4);
+      asm volatile("" : "+v"(ko));
+      return *reinterpret_cast<const bf16x8*>(kl + ko);
+    };
+    bf16x8 ka = kread(0), kn;
+#pragma unroll
+    for (int s = 0; s < C::kKsteps; ++s) {
+      if (s + 1 < C::kKsteps) kn = kread(s + 1);
+      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[s], sacc, 0, 0, 0);
+      ka = kn;
+    }
+    // sacc[v] = score of query qi with tile key 8 (v/4) + 4 g + v%4
+    {
+      const int lim_g = lim - 4 * g, lo_g = lo - 4 * g;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int kk = (v >> 2) * 8 + (v & 3);
+        if (kk > lim_g || kk < lo_g) sacc[v] = -INFINITY;
+      }
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[v]);
+    {
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+      mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));  // with lane ^ 32
+    }
+    const float m_new = fmaxf(m_run, mx * sc);
+    if (__any(m_new - m_run > kLazy)) {
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < C::kDtiles; ++dt)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) oacc[dt][v] *= alpha;
+      m_run = m_new;
+    }
+    float psum = 0.f;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const float p = __builtin_amdgcn_exp2f(fmaf(sacc[v], sc, -m_run));
+      sacc[v] = p;
+      psum += p;
+    }
+    l_run += psum;
+#pragma unroll
+    for (int m = 0; m < 2; ++m) {
+      bf16x8 pb;
+#pragma unroll
+      for (int v = 0; v < 8; ++v) pb[v] = (__bf16)sacc[8 * m + v];
+      const int r0 = 16 * m * C::kRB;
+#pragma unroll
+      for (int dt = 0; dt < C::kDtiles; ++dt) {
+        int vo = (4 * (grp >> 1) + ri) * C::kRB + 32 * (grp & 1) + 8 * bq + ((dt ^ (D == 128 ? ri : (ri >> 1) & 1)) << 6);
+        asm volatile("" : "+v"(vo));
+        const bf16x4 lo4 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vl + (vo + r0)));
+        const bf16x4 hi4 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vl + (vo + r0 + 8 * C::kRB)));
+        const bf16x8 a = __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7);
+        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, oacc[dt], 0, 0, 0);
+      }
+    }
+  };
+
+  // O and LSE of the finished query tile.
+  auto finish_q = [&]() __attribute__((always_inline)) {
+    float l_tot;
+    {
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(l_run), __float_as_uint(l_run), false, false);
+      l_tot = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);  // with lane ^ 32
+    }
+    if (wave_live) {
+      if (qi < T) {
+        const float inv = 1.f / l_tot;
+        __bf16* op = owin + (int64_t)qi * H * D + 4 * g;
+        // oacc[dt][4 v4 + e] = O[qi][32 dt + 8 v4 + 4 g + e]
+        auto w2 = [&](int dt, int v4) {
+          uint2 w;
+          w.x = focus::pack_bf16x2(oacc[dt][4 * v4 + 0] * inv, oacc[dt][4 * v4 + 1] * inv);
+          w.y = focus::pack_bf16x2(oacc[dt][4 * v4 + 2] * inv, oacc[dt][4 * v4 + 3] * inv);
+          return w;
+        };
+#pragma unroll
+        for (int dt = 0; dt < C::kDtiles; ++dt)
+#pragma unroll
+          for (int v4 = 0; v4 < 4; ++v4) *reinterpret_cast<uint2*>(op + 32 * dt + 8 * v4) = w2(dt, v4);
+        if (g == 0 && d.lse) d.lse[(tok0 + qi) * H + h] = (m_run + log2f(l_tot)) * kLn2;
+      }
+    }
+#pragma unroll
+    for (int dt = 0; dt < C::kDtiles; ++dt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) oacc[dt][v] = 0.f;
+    m_run = kMinit;
+    l_run = 0.f;
+  };
+
+  // Step u: copies of tile u + 4 into the stage tile u - 1 left, tile u
+  // computed, then this wave waits until its copies of tile u + 1 have landed
+  // (those of u + 2 .. u + 4 may stay in flight; O stores issued after them
+  // only make the wait stricter) and the barrier makes that true for every
+  // wave's share.
+  auto wait_next = [&]() __attribute__((always_inline)) {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(((3 * kPer) & 15) | (((3 * kPer) >> 4) << 14) | (7 << 4) | (15 << 8));
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  };
+  auto step = [&](int u, const char* kc, const char* vc, char* kn_, char* vn_) __attribute__((always_inline)) {
+    issue_next(kn_, vn_);
+    // First tile of query tile cq: the next one's Q starts loading, after this
+    // step's copies.
+    if (ct == 0 && cq + 1 < nqt) load_q_async<C::kKsteps>(q_row(cq + 1), qn);
+    compute_tile(kc, vc);
+    if (++ct == c_nt) {
+      if (cq + 1 < nqt) {
+        // Every query tile but the last has at least five tiles, so at least
+        // four steps' copies were issued after that Q: once no more than the
+        // copies of the four tiles in flight are outstanding, it has landed.
+        wait_loaded<4 * kPer>(qn);
+#pragma unroll
+        for (int s = 0; s < C::kKsteps; ++s) qf[s] = qn[s];
+      }
+      finish_q();
+      if (cq + 1 < nqt) {
+        ++cq;
+        ct = 0;
+        c_tw0 = tw0_of(cq);
+        c_nt = ntiles_of(cq);
+        set_q(cq);
+      }
+    }
+    if (u + 1 < nsteps) wait_next();
+  };
+
+  load_q_now<C::kKsteps>(q_row(0), qf);
+  set_q(0);
+  issue_next(kb0, vb0);
+  issue_next(kb1, vb1);
+  issue_next(kb2, vb2);
+  issue_next(kb3, vb3);
+  wait_next();  // tile 0 has landed
+  for (int u = 0; u < nsteps; u += 5) {
+    step(u, kb0, vb0, kb4, vb4);
+    if (u + 1 >= nsteps) break;
+    step(u + 1, kb1, vb1, kb0, vb0);
+    if (u + 2 >= nsteps) break;
+    step(u + 2, kb2, vb2, kb1, vb1);
+    if (u + 3 >= nsteps) break;
+    step(u + 3, kb3, vb3, kb2, vb2);
+    if (u + 4 >= nsteps) break;
+    step(u + 4, kb4, vb4, kb3, vb3);
+  }
+  // No copy may still be writing this workgroup's LDS when it ends (and the
+  // last O stores complete).
+  __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
 }
 
 // ------------------------------------------- bf16 MFMA, C(t), pipelined waves
@@ -1678,12 +2067,14 @@ extern "C" focus_status focus_window_attn(const focus_attn_desc* d, focus_stream
   const dim3 grid((uint32_t)blocks), block(threads);
 #define FOCUS_ATTN_LAUNCH(KERNEL) hipLaunchKernelGGL(KERNEL, grid, block, 0, s, *d, sc, n_pairs, (int)qt, SumQ{})
 #define FOCUS_CT_LAUNCH(KERNEL) hipLaunchKernelGGL(KERNEL, grid, block, 0, s, *d, sc, n_pairs, (int)qt, sp)
+// k-mer-local bf16: one workgroup per (window, head), looping over its query tiles.
+#define FOCUS_KL_LAUNCH(KERNEL) hipLaunchKernelGGL(KERNEL, dim3((uint32_t)n_pairs), dim3(256), 0, s, *d, sc, n_pairs)
 #define FOCUS_F32_LAUNCH(KERNEL) hipLaunchKernelGGL(KERNEL, grid, block, 0, s, *d, sc, n_pairs, (int)qt, SumQ{})
   if (d->dtype == FOCUS_BF16) {
     if (d->head_dim == 128) {
-      if (kl) FOCUS_ATTN_LAUNCH((attn_bf16<128, kBf16WavesKL, true, false>)); else FOCUS_CT_LAUNCH((attn_ct<128>));
+      if (kl) FOCUS_KL_LAUNCH((attn_kl<128>)); else FOCUS_CT_LAUNCH((attn_ct<128>));
     } else {
-      if (kl) FOCUS_ATTN_LAUNCH((attn_bf16<64, kBf16WavesKL, true, false>)); else FOCUS_CT_LAUNCH((attn_ct<64>));
+      if (kl) FOCUS_KL_LAUNCH((attn_kl<64>)); else FOCUS_CT_LAUNCH((attn_ct<64>));
     }
     if (sp.n > 1) {
       const int64_t lanes = sp.nwl * sp.rows * d->n_heads * (d->head_dim / 4);
