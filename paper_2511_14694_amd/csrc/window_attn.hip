@@ -633,8 +633,9 @@ __device__ __forceinline__ void wait_loaded(bf16x8 (&q)[NS]) {
 // The k-mer-local window attention (Section 3.2 rule): one workgroup streams a
 // whole (window, head).  Its 4 waves x 32 rows take the window's 128-row query
 // tiles one after another, and the key tiles of all of them form one stream of
-// 32-key tiles through five LDS stages, four in flight while one is computed
-// (80 KB: two workgroups fill a compute unit's LDS).
+// 32-key tiles through four LDS stages, three in flight while one is computed;
+// a one-tile summary list stays in LDS for all query tiles (80 KB in all: two
+// workgroups fill a compute unit's LDS).
 // Query tile q visits the gathered summary list [carried boundary ; the
 // window's summaries] and then the window tiles from the one holding the first
 // row of its first k-mer up to its last row, with a two-sided mask keeping each
@@ -646,8 +647,9 @@ __device__ __forceinline__ void wait_loaded(bf16x8 (&q)[NS]) {
 template <int D>
 __global__ __launch_bounds__(256, 2) void attn_kl(focus_attn_desc d, float sc, int64_t n_pairs) {
   using C = Cfg<D, 4, 32>;
-  __shared__ __attribute__((aligned(1024))) char kb0[C::kTile], kb1[C::kTile], kb2[C::kTile], kb3[C::kTile], kb4[C::kTile];
-  __shared__ __attribute__((aligned(1024))) char vb0[C::kTile], vb1[C::kTile], vb2[C::kTile], vb3[C::kTile], vb4[C::kTile];
+  __shared__ __attribute__((aligned(1024))) char kb0[C::kTile], kb1[C::kTile], kb2[C::kTile], kb3[C::kTile];
+  __shared__ __attribute__((aligned(1024))) char vb0[C::kTile], vb1[C::kTile], vb2[C::kTile], vb3[C::kTile];
+  __shared__ __attribute__((aligned(1024))) char kls[C::kTile], vls[C::kTile];  // resident summary list
 
   const int tid = threadIdx.x;
   // Block -> (listed window, head), heads fastest: the workgroups running at
@@ -678,11 +680,16 @@ __global__ __launch_bounds__(256, 2) void attn_kl(focus_attn_desc d, float sc, i
   const int nsum = kw > 0 ? (T + kw) / (kw + 1) : 0;
   const int nct = (nsum + C::kBK) / C::kBK;  // tiles of the summary list (boundary + nsum)
   const int nqt = (T + C::kBQ - 1) / C::kBQ;
+  // A one-tile summary list (up to 31 summaries: k >= 32 at windows of 1000)
+  // is copied once and stays in LDS; a longer one is streamed again for each
+  // query tile (nl of its tiles in the stream).
+  const bool resident = nct == 1;
+  const int nl = resident ? 0 : nct;
   // Query tile q: its first window tile (the one holding the first row of its
   // first k-mer), the window keys it can see and its tile count.
   auto tw0_of = [&](int q) { return kw > 0 ? q * C::kBQ / (kw + 1) * (kw + 1) / C::kBK : 0; };
   auto nwk_of = [&](int q) { return min(q * C::kBQ + C::kBQ, T); };
-  auto ntiles_of = [&](int q) { return nct + (nwk_of(q) + C::kBK - 1) / C::kBK - tw0_of(q); };
+  auto ntiles_of = [&](int q) { return nl + (nwk_of(q) + C::kBK - 1) / C::kBK - tw0_of(q); };
   int nsteps = 0;
   for (int q = 0; q < nqt; ++q) nsteps += ntiles_of(q);
 
@@ -720,25 +727,38 @@ __global__ __launch_bounds__(256, 2) void attn_kl(focus_attn_desc d, float sc, i
 
   // Issue side: the next tile of the stream (query tile iq, its tile it_).
   int iq = 0, it_ = 0, i_tw0 = tw0_of(0), i_nwk = nwk_of(0), i_nt = ntiles_of(0);
+  // Summary-list entry R = 32 t + r: R = 0 is the carried boundary, R >= 1
+  // the window's summary R - 1 at window row R (k + 1) - 1 (the last one at
+  // T - 1).  Rows past the list repeat its last entry (masked).
+  auto list_src = [&](int t, const char** ks, const char** vs) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < kDma; ++i) {
+      const int r = (wave * kDma + i) * kRPK + lane / C::kCh16;
+      const int R = min(t * C::kBK + r, nsum);
+      const bool boundary = R == 0 && Cw > 0;
+      const int wrow = R == 0 ? 0 : min(R * (kw + 1) - 1, T - 1);
+      ks[i] = (boundary ? kcache + (int64_t)(Cw - 1) * row_bytes : kwin + (int64_t)wrow * row_bytes) + kchunk[i];
+      vs[i] = (boundary ? vcache + (int64_t)(Cw - 1) * row_bytes : vwin + (int64_t)wrow * row_bytes) + vchunk[i];
+    }
+  };
+  // This wave's share of a tile: one copy pair per 1 KB.
+  auto copy_tile = [&](const char* const* ks, const char* const* vs, char* kbuf, char* vbuf)
+      __attribute__((always_inline)) {
+    const uint32_t kl = lds_addr(kbuf) + wave * kDma * 1024;
+    const uint32_t vl = lds_addr(vbuf) + wave * kDma * 1024;
+#pragma unroll
+    for (int i = 0; i < kDma; ++i) {
+      copy_to_lds(ks[i], kl + i * 1024);
+      copy_to_lds(vs[i], vl + i * 1024);
+    }
+  };
   auto issue_next = [&](char* kbuf, char* vbuf) __attribute__((always_inline)) {
-    // Per-lane source rows of this wave's share, then one copy pair per 1 KB.
     const char* ks[kDma];
     const char* vs[kDma];
-    if (it_ < nct) {
-      // Summary-list entry R = 32 t + r: R = 0 is the carried boundary, R >= 1
-      // the window's summary R - 1 at window row R (k + 1) - 1 (the last one at
-      // T - 1).  Rows past the list repeat its last entry (masked).
-#pragma unroll
-      for (int i = 0; i < kDma; ++i) {
-        const int r = (wave * kDma + i) * kRPK + lane / C::kCh16;
-        const int R = min(it_ * C::kBK + r, nsum);
-        const bool boundary = R == 0 && Cw > 0;
-        const int wrow = R == 0 ? 0 : min(R * (kw + 1) - 1, T - 1);
-        ks[i] = (boundary ? kcache + (int64_t)(Cw - 1) * row_bytes : kwin + (int64_t)wrow * row_bytes) + kchunk[i];
-        vs[i] = (boundary ? vcache + (int64_t)(Cw - 1) * row_bytes : vwin + (int64_t)wrow * row_bytes) + vchunk[i];
-      }
+    if (it_ < nl) {
+      list_src(it_, ks, vs);
     } else {
-      const int row0 = (it_ - nct + i_tw0) * C::kBK;
+      const int row0 = (it_ - nl + i_tw0) * C::kBK;
       const int nvalid = i_nwk - row0;
       const char* kb = kwin + (int64_t)row0 * row_bytes;
       const char* vb = vwin + (int64_t)row0 * row_bytes;
@@ -750,13 +770,7 @@ __global__ __launch_bounds__(256, 2) void attn_kl(focus_attn_desc d, float sc, i
         vs[i] = vb + (rb + vchunk[i]);
       }
     }
-    const uint32_t kl = lds_addr(kbuf) + wave * kDma * 1024;
-    const uint32_t vl = lds_addr(vbuf) + wave * kDma * 1024;
-#pragma unroll
-    for (int i = 0; i < kDma; ++i) {
-      copy_to_lds(ks[i], kl + i * 1024);
-      copy_to_lds(vs[i], vl + i * 1024);
-    }
+    copy_tile(ks, vs, kbuf, vbuf);
     if (it_ + 1 < i_nt) {
       ++it_;
     } else if (iq + 1 < nqt) {
@@ -792,9 +806,9 @@ __global__ __launch_bounds__(256, 2) void attn_kl(focus_attn_desc d, float sc, i
   bf16x8 qf[C::kKsteps], qn[C::kKsteps];
   const int grp = lane >> 4, ri = (lane >> 2) & 3, bq = lane & 3;
 
-  auto compute_tile = [&](const char* kl, const char* vl) __attribute__((always_inline)) {
-    const bool in_list = ct < nct;
-    const int row0 = in_list ? ct * C::kBK : (ct - nct + c_tw0) * C::kBK;
+  // One tile of keys: the summary list's entries row0 .. row0 + 31 (in_list),
+  // else window rows row0 .. row0 + 31.
+  auto compute_tile = [&](const char* kl, const char* vl, bool in_list, int row0) __attribute__((always_inline)) {
     const bool live = wave_live && (in_list || (row0 <= wq_lo + 31 && row0 + C::kBK > klo_w));
     // visible tile keys: lo <= kk <= lim
     const int lim = in_list ? jq - row0 : qi - row0;
@@ -901,14 +915,15 @@ __global__ __launch_bounds__(256, 2) void attn_kl(focus_attn_desc d, float sc, i
     l_run = 0.f;
   };
 
-  // Step u: copies of tile u + 4 into the stage tile u - 1 left, tile u
-  // computed, then this wave waits until its copies of tile u + 1 have landed
-  // (those of u + 2 .. u + 4 may stay in flight; O stores issued after them
+  // Step u: copies of tile u + 3 into the stage tile u - 1 left, tile u
+  // computed (after the resident summary list, at a query tile's first
+  // step), then this wave waits until its copies of tile u + 1 have landed
+  // (those of u + 2 and u + 3 may stay in flight; O stores issued after them
   // only make the wait stricter) and the barrier makes that true for every
   // wave's share.
   auto wait_next = [&]() __attribute__((always_inline)) {
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    __builtin_amdgcn_s_waitcnt(((3 * kPer) & 15) | (((3 * kPer) >> 4) << 14) | (7 << 4) | (15 << 8));
+    __builtin_amdgcn_s_waitcnt(((2 * kPer) & 15) | (((2 * kPer) >> 4) << 14) | (7 << 4) | (15 << 8));
     __builtin_amdgcn_s_barrier();
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
   };
@@ -917,13 +932,15 @@ __global__ __launch_bounds__(256, 2) void attn_kl(focus_attn_desc d, float sc, i
     // First tile of query tile cq: the next one's Q starts loading, after this
     // step's copies.
     if (ct == 0 && cq + 1 < nqt) load_q_async<C::kKsteps>(q_row(cq + 1), qn);
-    compute_tile(kc, vc);
+    if (ct == 0 && resident) compute_tile(kls, vls, true, 0);
+    compute_tile(kc, vc, ct < nl, ct < nl ? ct * C::kBK : (ct - nl + c_tw0) * C::kBK);
     if (++ct == c_nt) {
       if (cq + 1 < nqt) {
-        // Every query tile but the last has at least five tiles, so at least
-        // four steps' copies were issued after that Q: once no more than the
-        // copies of the four tiles in flight are outstanding, it has landed.
-        wait_loaded<4 * kPer>(qn);
+        // Every query tile but the last streams at least four tiles, so at
+        // least three steps' copies were issued after that Q: once no more
+        // than the copies of the three tiles in flight are outstanding, it has
+        // landed.
+        wait_loaded<3 * kPer>(qn);
 #pragma unroll
         for (int s = 0; s < C::kKsteps; ++s) qf[s] = qn[s];
       }
@@ -941,21 +958,24 @@ __global__ __launch_bounds__(256, 2) void attn_kl(focus_attn_desc d, float sc, i
 
   load_q_now<C::kKsteps>(q_row(0), qf);
   set_q(0);
+  if (resident) {
+    const char* ks[kDma];
+    const char* vs[kDma];
+    list_src(0, ks, vs);
+    copy_tile(ks, vs, kls, vls);
+  }
   issue_next(kb0, vb0);
   issue_next(kb1, vb1);
   issue_next(kb2, vb2);
-  issue_next(kb3, vb3);
-  wait_next();  // tile 0 has landed
-  for (int u = 0; u < nsteps; u += 5) {
-    step(u, kb0, vb0, kb4, vb4);
+  wait_next();  // the summary list and tile 0 have landed
+  for (int u = 0; u < nsteps; u += 4) {
+    step(u, kb0, vb0, kb3, vb3);
     if (u + 1 >= nsteps) break;
     step(u + 1, kb1, vb1, kb0, vb0);
     if (u + 2 >= nsteps) break;
     step(u + 2, kb2, vb2, kb1, vb1);
     if (u + 3 >= nsteps) break;
     step(u + 3, kb3, vb3, kb2, vb2);
-    if (u + 4 >= nsteps) break;
-    step(u + 4, kb4, vb4, kb3, vb3);
   }
   // No copy may still be writing this workgroup's LDS when it ends (and the
   // last O stores complete).

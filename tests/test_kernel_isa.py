@@ -2,7 +2,7 @@
 
 attn_kl loads the next query tile's Q with inline-assembly global loads that
 it does not wait for at once: the registers are written when the loads land,
-and the kernel's own waits (at least four steps later) cover them.  That is
+and the kernel's own waits (at least three steps later) cover them.  That is
 only correct while the compiler leaves those registers alone until the copy
 at the query-tile boundary (no spill, no move, no other use).  Its global ->
 LDS copies are inline assembly too, so the compiler inserts no wait of its own
@@ -74,9 +74,9 @@ def test_prefetched_q_registers_untouched_until_copied(asm, head_dim):
         i += 1
     assert blocks > 0, "no asynchronous Q load found"
     assert len(prefetch) == 4 * (head_dim // 16)
-    # Copies of tiles in flight at a query-tile boundary: four steps' copies of
-    # 2 x (tile bytes / 1 KB / 4 waves) each.
-    in_flight = 4 * 2 * (32 * head_dim * 2 // 1024 // 4)
+    # Copies of the tiles in flight at a query-tile boundary: three steps'
+    # copies of 2 x (tile bytes / 1 KB / 4 waves) each.
+    in_flight = 3 * 2 * (32 * head_dim * 2 // 1024 // 4)
     uses = 0
     in_asm = False
     last_wait = None  # vmcnt of the latest s_waitcnt in layout order
