@@ -520,9 +520,6 @@ __global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_d
 
 // ------------------------------------------------- bf16 MFMA, k-mer-local
 
-// q[s] = p[2 s] (16 bytes each, 32 bytes apart) for s < NS, returned only once
-// every vector memory operation of this wave has completed (the wait is part
-// of the statement, so the compiler tracks no load in flight into q).
 // The k-mer-local kernel below issues its global -> LDS copies as inline
 // assembly, so the compiler does not track them: with the compiler-visible
 // copy in this loop's control flow it conservatively waits for every copy in
@@ -530,7 +527,9 @@ __global__ __launch_bounds__(64 * W, W == 1 ? 1 : 2) void attn_bf16(focus_attn_d
 // instead of three.  The kernel's own waits (a vmcnt wait and a barrier that
 // close each step) order every LDS read after the copies it needs.
 //
-// 16 bytes per lane from src to LDS byte lds + 16 lane (one wave: 1 KB).
+// 16 bytes per lane from src to LDS byte lds + 16 lane (one wave: 1 KB); lds
+// goes in M0, which the compiler writes just before, so the copy waits one
+// cycle for it (s_nop 0).
 __device__ __forceinline__ void copy_to_lds(const void* src, uint32_t lds) {
   asm volatile(
       "s_nop 0\n\t"
@@ -544,6 +543,9 @@ __device__ __forceinline__ uint32_t lds_addr(const char* p) {
   return (uint32_t)(uintptr_t)(lds_char*)p;
 }
 
+// q[s] = p[2 s] (16 bytes each, 32 bytes apart) for s < NS, returned only once
+// every vector memory operation of this wave has completed (the wait is part
+// of the statement, so the compiler tracks no load in flight into q).
 template <int NS>
 __device__ __forceinline__ void load_q_now(const bf16x8* p, bf16x8 (&q)[NS]) {
   static_assert(NS == 4 || NS == 8, "head_dim 64 or 128");
