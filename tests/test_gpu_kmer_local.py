@@ -3,7 +3,8 @@ visibility rule) against the float64 oracle.
 
 Small cases compare every output row (several query tiles, ragged tails, GQA,
 head_dim 64 and 128, k = 0 windows, k = 1, partial k-mers, windows with more
-than 64 summaries); the 1 Mb and ragged workloads at full size run one
+than 64 summaries, a summary list that exactly fills one 32-row tile, query
+tiles of exactly four window tiles); the 1 Mb and ragged workloads at full size run one
 masked-parallel launch and compare sampled windows and heads.  Properties on
 the device output: every softmax row sums to one over the k-mer-local visible
 set through the returned LSE, streaming equals masked-parallel bit for bit, and
@@ -61,6 +62,8 @@ SMALL_KL = [
     ([1], 1000, 100, 4, 4, 128),
     ([130, 129, 64], 1000, 1, 2, 2, 128),   # k = 1: 2-token k-mers, > 64 summaries
     ([2600], 1300, 9, 2, 2, 128),       # 130 summaries per window: three list tiles
+    ([2000], 1000, 127, 2, 2, 128),     # k-mers of 128 rows: four window tiles per query tile
+    ([1000, 1000], 1000, 33, 2, 1, 128),  # 31 summaries: the boundary and list fill one tile
 ]
 
 
