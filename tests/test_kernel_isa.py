@@ -2,7 +2,7 @@
 
 attn_kl loads the next query tile's Q with inline-assembly global loads that
 it does not wait for at once: the registers are written when the loads land,
-and the kernel's own waits (at least three steps later) cover them.  That is
+and the kernel's own waits (a stage count of steps later) cover them.  That is
 only correct while the compiler leaves those registers alone until the copy
 at the query-tile boundary (no spill, no move, no other use).  Its global ->
 LDS copies are inline assembly too, so the compiler inserts no wait of its own
@@ -19,9 +19,10 @@ import pytest
 
 from paper_2511_14694_amd import build as B
 
+# head_dim -> (symbol, waves per workgroup, LDS stages) of the instantiations
 KERNELS = {
-    128: "_ZN12_GLOBAL__N_17attn_klILi128EEEv15focus_attn_descfl",
-    64: "_ZN12_GLOBAL__N_17attn_klILi64EEEv15focus_attn_descfl",
+    128: ("_ZN12_GLOBAL__N_17attn_klILi128ELi4ELi4EEEv15focus_attn_descfl", 4, 4),
+    64: ("_ZN12_GLOBAL__N_17attn_klILi64ELi4ELi4EEEv15focus_attn_descfl", 4, 4),
 }
 
 
@@ -55,7 +56,8 @@ def _regs(text):
 
 @pytest.mark.parametrize("head_dim", [128, 64])
 def test_prefetched_q_registers_untouched_until_copied(asm, head_dim):
-    start, end = _body(asm, KERNELS[head_dim])
+    name, waves, stages = KERNELS[head_dim]
+    start, end = _body(asm, name)
     # the asynchronous Q loads: inline-assembly blocks of plain global loads
     # with no wait inside
     prefetch, blocks = set(), 0
@@ -74,9 +76,9 @@ def test_prefetched_q_registers_untouched_until_copied(asm, head_dim):
         i += 1
     assert blocks > 0, "no asynchronous Q load found"
     assert len(prefetch) == 4 * (head_dim // 16)
-    # Copies of the tiles in flight at a query-tile boundary: three steps'
-    # copies of 2 x (tile bytes / 1 KB / 4 waves) each.
-    in_flight = 3 * 2 * (32 * head_dim * 2 // 1024 // 4)
+    # Copies of the tiles in flight at a query-tile boundary: (stages - 1)
+    # steps' copies of 2 x (tile bytes / 1 KB / waves) each.
+    in_flight = (stages - 1) * 2 * (32 * head_dim * 2 // 1024 // waves)
     uses = 0
     in_asm = False
     last_wait = None  # vmcnt of the latest s_waitcnt in layout order
@@ -105,7 +107,7 @@ def test_prefetched_q_registers_untouched_until_copied(asm, head_dim):
 
 @pytest.mark.parametrize("head_dim", [128, 64])
 def test_no_spills_and_no_compiler_wait_before_lds_reads(asm, head_dim):
-    name = KERNELS[head_dim]
+    name = KERNELS[head_dim][0]
     # kernel metadata: the fields after .name are in alphabetical order
     i = next(k for k, line in enumerate(asm) if re.search(r"\.name:\s+" + re.escape(name) + r"$", line))
     spill = next(line for line in asm[i:] if ".vgpr_spill_count:" in line)
